@@ -1,0 +1,165 @@
+"""Closed-formula tile derivation for fused attention (model of the C++ routine).
+
+Test infrastructure only.  Written from Sections 3-5 of the paper, applied in
+the paper's CU-centric order (Section 4):
+
+1. LDS -> KV tile.  The staged K/V tiles must fit the LDS share the kernel
+   structure gives them: t_KV = floor(share / (kv_tiles * d * elem)), aligned
+   down to the atom (Section 4, "LDS constraint" and "Atom alignment").  The
+   paper's attention instance gives half of LDS to one streamed t_KV x d tile
+   (Table 2: t_KV = 64 at d=128, 128 at d=64 with fp32 elements).
+2. VGPR -> Q tile per wave.  Every array live at the synchronisation point
+   between the two GEMMs is counted (Section 5.2, Table 2 caption): the Q
+   operand, the fp32 score tile, the fp32 output accumulator and the running
+   (m, delta) pair, plus the registers used to stage the next K/V tile and a
+   fixed overhead.  t_Q is the largest multiple of the atom width whose count
+   fits the per-wave budget (Section 4, "VGPR constraint").  The count
+   reproduces all four rows of Table 2 with the paper's fp32 instance.
+3. CU count -> grid.  If fewer workgroups than CUs result, the derivation
+   splits the key range (the merge of Section 4.3 is associative), then
+   reduces the Q tile -- waves per workgroup first, then rows per wave --
+   until every CU has a workgroup or the tile is one atom (Section 4,
+   "Occupancy constraint").
+4. Atom alignment of every tile dimension (Section 4).
+
+All quantities are integers; the result is unique for its inputs.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+
+
+@dataclasses.dataclass(frozen=True)
+class Hardware:
+    lds_bytes: int
+    vgpr_per_thread: int
+    wavefront_size: int
+    num_cus: int
+    simds_per_cu: int = 4
+    lds_bytes_per_clk: int = 0
+    mfma_flops_per_clk_cu: int = 0
+
+
+@dataclasses.dataclass(frozen=True)
+class Atom:
+    m: int
+    n: int
+    k: int
+    in_bytes: int
+    acc_bytes: int
+
+
+@dataclasses.dataclass(frozen=True)
+class Op:
+    B: int
+    H: int
+    L: int
+    d: int
+    elem_bytes: int
+    causal: bool = False
+
+
+@dataclasses.dataclass(frozen=True)
+class Structure:
+    """Fixed properties of one kernel family (chosen once, never searched)."""
+    kv_lds_num: int = 1      # share of LDS that holds staged K/V tiles ...
+    kv_lds_den: int = 1      # ... as the fraction num/den
+    kv_tiles: int = 1        # t_KV x d tiles resident in that share
+    stage_tiles: int = 0     # t_KV x d tiles passed through VGPRs per step
+    waves_per_wg: int = 1
+    waves_per_simd: int = 1  # resident waves per SIMD (divides the register file)
+    vgpr_fixed: int = 16     # addresses, loop state, operand staging
+    max_split: int = 1       # key-range splits allowed by the CU rule
+
+
+def _cdiv(a, b):
+    return -(-a // b)
+
+
+def vgpr_count(hw, atom, op, st, t_q, t_kv, n_w):
+    """Registers per lane live at the GEMM1/GEMM2 synchronisation point."""
+    wf = hw.wavefront_size
+    q_reg = _cdiv(t_q * op.d * op.elem_bytes, 4 * wf)        # Q operand
+    s_reg = _cdiv(t_q * t_kv * atom.acc_bytes, 4 * wf)       # score tile, fp32
+    o_reg = _cdiv(t_q * op.d * atom.acc_bytes, 4 * wf)       # output accumulator, fp32
+    stats = 2 * _cdiv(t_q, atom.n)                           # running max and sum
+    stage = _cdiv(st.stage_tiles * t_kv * op.d * op.elem_bytes, 4 * wf * n_w)
+    return q_reg + s_reg + o_reg + stats + stage + st.vgpr_fixed
+
+
+def derive(hw, atom, op, st):
+    """Return a dict with the tiles, the grid and the feasibility report."""
+    rep = dict(feasible=False, binding="", t_kv=0, t_q_wave=0, n_waves=0, tile_q=0,
+               n_split=1, grid=0, vgpr_est=0, vgpr_budget=0, lds_used=0, lds_budget=0,
+               wg_per_cu=0.0, low_occupancy=True, lds_bw_ok=True)
+    align_kv = math.lcm(atom.n, atom.k)
+    align_q = atom.n
+    lds_share = hw.lds_bytes * st.kv_lds_num // st.kv_lds_den
+    rep["lds_budget"] = lds_share
+    budget = hw.vgpr_per_thread // st.waves_per_simd
+    rep["vgpr_budget"] = budget
+
+    # 4 (checked first because the others assume it): the contraction over d
+    # and the d-rows of the second product must be whole atoms.
+    if op.d % atom.k or op.d % atom.m:
+        rep["binding"] = "atom"
+        return rep
+
+    # 1. LDS -> t_KV
+    t_kv = lds_share // (st.kv_tiles * op.d * op.elem_bytes)
+    t_kv -= t_kv % align_kv
+    if t_kv <= 0:
+        rep["binding"] = "LDS"
+        return rep
+    rep["t_kv"] = t_kv
+    rep["lds_used"] = st.kv_tiles * t_kv * op.d * op.elem_bytes
+
+    # 2. VGPR -> t_Q per wave: the largest aligned size whose live set fits.
+    n_w = st.waves_per_wg
+    t_q = 0
+    cand = align_q
+    while vgpr_count(hw, atom, op, st, cand, t_kv, n_w) <= budget:
+        t_q = cand
+        cand += align_q
+    if t_q == 0:
+        rep["binding"] = "VGPR"
+        rep["vgpr_est"] = vgpr_count(hw, atom, op, st, align_q, t_kv, n_w)
+        return rep
+
+    # 3. CU count -> grid.
+    binding = "VGPR"
+    n_kv = _cdiv(op.L, t_kv)
+    n_qt = _cdiv(op.L, n_w * t_q)
+    heads = op.B * op.H
+    n_split = 1
+    if heads * n_qt < hw.num_cus and st.max_split > 1:
+        need = _cdiv(hw.num_cus, heads * n_qt)
+        want = 1
+        while want < need:
+            want *= 2
+        n_split = min(want, st.max_split, n_kv)
+        n_split = _cdiv(n_kv, _cdiv(n_kv, n_split))   # drop empty splits
+        if n_split > 1:
+            binding = "CU"
+    # Still fewer workgroups than CUs: shrink the Q tile, first by halving the
+    # waves per workgroup (if the registers that staging needs per lane still
+    # fit), else by one atom step of the per-wave tile.
+    while heads * n_qt * n_split < hw.num_cus:
+        if n_w > 1 and vgpr_count(hw, atom, op, st, t_q, t_kv, n_w // 2) <= budget:
+            n_w //= 2
+        elif t_q > align_q:
+            t_q -= align_q
+        else:
+            break
+        n_qt = _cdiv(op.L, n_w * t_q)
+        binding = "CU"
+
+    grid = heads * n_qt * n_split
+    rep.update(feasible=True, binding=binding, t_q_wave=t_q, n_waves=n_w, tile_q=n_w * t_q,
+               n_split=n_split, grid=grid,
+               vgpr_est=vgpr_count(hw, atom, op, st, t_q, t_kv, n_w),
+               wg_per_cu=grid / hw.num_cus, low_occupancy=grid < hw.num_cus)
+    if hw.lds_bytes_per_clk > 0 and hw.mfma_flops_per_clk_cu > 0:
+        rep["lds_bw_ok"] = t_q * hw.lds_bytes_per_clk >= hw.mfma_flops_per_clk_cu
+    return rep
