@@ -1,0 +1,181 @@
+/*
+ * Fused attention forward for AMD MI355X (gfx950 / CDNA4): C ABI.
+ *
+ * The library computes O = softmax(scale * Q K^T) V per (batch, head) as two
+ * chained matrix-core products with an online softmax between them, so the
+ * L x L score matrix never reaches device memory (paper: Section 5, the
+ * attention equation, Algorithm 1 and Figure 2).  Tile sizes come from a
+ * closed-formula derivation over a hardware descriptor (Sections 3 and 4,
+ * Table 2); nothing is searched or tuned at run time.
+ *
+ * Conventions for every entry point:
+ *  - Return value: 0 (ATTN_OK) on success, a negative attn_status_t on error.
+ *    attn_strerror() names the code.  Arguments are validated before any HIP
+ *    call is made, so a rejected call has no device side effect.
+ *  - Tensors Q, K, V, O: device pointers to contiguous [B, H, L, d] arrays
+ *    (d innermost), element type given by `dtype`; each (b, h) slice is the
+ *    paper's row-major L x d matrix.  O has the same type as the inputs.
+ *    Every tensor base address must be 16-byte aligned.
+ *  - The caller owns every buffer it passes.  Calls are asynchronous: they
+ *    enqueue work on `stream` (a hipStream_t; NULL is the null stream) and
+ *    return without synchronising.  Inputs must stay valid until that work
+ *    completes.
+ *  - Sizes: 1 <= B, H; 1 <= L <= ATTN_MAX_L; d in {64, 128};
+ *    B * H * L * d < 2^62.
+ */
+#ifndef PAPER_2609_10937_ATTN_H
+#define PAPER_2609_10937_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ATTN_MAX_L (1 << 24)
+
+typedef enum { ATTN_BF16 = 0, ATTN_F16 = 1 } attn_dtype_t;
+
+typedef enum {
+  ATTN_OK = 0,
+  ATTN_E_NULLPTR = -1,        /* a required pointer is NULL */
+  ATTN_E_SHAPE = -2,          /* B, H or L outside the supported range */
+  ATTN_E_UNSUPPORTED_D = -3,  /* head dimension not in {64, 128} */
+  ATTN_E_DTYPE = -4,          /* dtype not an attn_dtype_t */
+  ATTN_E_ALIGN = -5,          /* a tensor base address is not 16-byte aligned */
+  ATTN_E_INFEASIBLE = -6,     /* tile derivation found no feasible tile (report.binding says why) */
+  ATTN_E_NO_INSTANCE = -7,    /* derived tiles have no compiled kernel; never falls back */
+  ATTN_E_HIP = -8,            /* a HIP runtime call failed */
+  ATTN_E_WORKSPACE = -9,      /* workspace missing or smaller than required */
+  ATTN_E_SCALE = -10,         /* scale is negative, NaN or infinite */
+  ATTN_E_ARG = -11,           /* other invalid argument (descriptor field, preset name, atom id) */
+  ATTN_E_DEVICE = -12         /* the current device is not a usable gfx950 GPU */
+} attn_status_t;
+
+/* One matrix-core instruction shape (Section 3, MFMAAtom): D[m x n] += A[m x k] B[k x n],
+ * inputs of in_bytes each, accumulation in acc_bytes. */
+typedef struct {
+  int32_t m, n, k;
+  int32_t in_bytes, acc_bytes;
+} attn_mfma_atom_t;
+
+/* Hardware descriptor (Section 3, HardwareDescriptor): only the quantities the
+ * derivation reads, plus peak figures used for reporting. */
+typedef struct {
+  int64_t lds_bytes;            /* LDS per CU (bytes) */
+  int32_t vgpr_per_thread;      /* registers per lane at one wave per SIMD */
+  int32_t wavefront_size;
+  int32_t num_cus;
+  int32_t simds_per_cu;
+  int32_t lds_bytes_per_clk;    /* LDS read bandwidth per CU (0 = unknown) */
+  int32_t mfma_flops_per_clk_cu;/* dense matrix-core flops per clock per CU (0 = unknown) */
+  double hbm_tbps;              /* HBM bandwidth, TB/s */
+  double peak_tflops;           /* dense matrix-core peak for the atom's input type */
+  double clock_ghz;
+  char name[32];
+} attn_hw_desc_t;
+
+/* The operation plus the fixed structure of the kernel family that will run it.
+ * The structure fields are properties of a kernel design, chosen once; the
+ * derivation never varies them. */
+typedef struct {
+  int32_t B, H, L, d;
+  int32_t elem_bytes;           /* bytes per Q/K/V element */
+  int32_t causal;
+  int32_t kv_lds_num, kv_lds_den; /* share of LDS given to staged K/V tiles */
+  int32_t kv_tiles;             /* t_KV x d tiles resident in that share */
+  int32_t stage_tiles;          /* t_KV x d tiles staged through registers per step */
+  int32_t waves_per_wg;
+  int32_t waves_per_simd;       /* resident waves per SIMD; divides the register file */
+  int32_t vgpr_fixed;           /* registers per lane outside the counted arrays */
+  int32_t max_split;            /* key-range splits the CU rule may use (1 = none) */
+} attn_op_t;
+
+/* Result of the derivation (Section 4: tiles, feasibility, binding constraint). */
+typedef struct {
+  int32_t feasible;
+  int32_t t_kv;                 /* key/value rows per tile (fixed by LDS) */
+  int32_t t_q_wave;             /* query rows per wave (fixed by registers) */
+  int32_t n_waves;              /* waves per workgroup */
+  int32_t tile_q;               /* query rows per workgroup = n_waves * t_q_wave */
+  int32_t n_split;              /* key-range splits (1 = none) */
+  int64_t grid;                 /* workgroups launched by the fused kernel */
+  int32_t vgpr_est, vgpr_budget;/* registers per lane at the GEMM1/GEMM2 sync point */
+  int64_t lds_used, lds_budget;
+  double wg_per_cu;
+  int32_t low_occupancy;        /* grid < num_cus */
+  int32_t lds_bw_ok;            /* t_q_wave * lds_bytes_per_clk >= mfma_flops_per_clk_cu */
+  char binding[16];             /* "LDS", "VGPR", "CU" or "atom" */
+} attn_tile_report_t;
+
+/* Fill `out` with a named descriptor: "paper_gpu_a" and "paper_gpu_b" (the two
+ * CDNA descriptors of Section 3), or "gfx950" (MI355X public figures).
+ * ATTN_E_ARG for an unknown name. */
+int attn_hw_desc_preset(const char* name, attn_hw_desc_t* out);
+
+/* Descriptor of HIP device `device`: CU count, LDS size, wavefront size and
+ * clock from the runtime, the rest from the gfx950 figures.  ATTN_E_DEVICE if
+ * the device is not gfx950, ATTN_E_HIP if the runtime cannot be queried. */
+int attn_hw_desc_query(int device, attn_hw_desc_t* out);
+
+/* Named atoms: "f32_16x16x4" (the paper's), "bf16_16x16x32", "f16_16x16x32". */
+int attn_atom_preset(const char* name, attn_mfma_atom_t* out);
+
+/* Fill `out` with the operation (B, H, L, d, dtype, causal) and the structure
+ * of this library's fused kernel family.  Same argument checks as attn_fwd. */
+int attn_fwd_op(int B, int H, int L, int d, int causal, int dtype, attn_op_t* out);
+
+/* Registers per lane live at the GEMM1/GEMM2 synchronisation point for a
+ * given (t_q per wave, t_kv, waves per workgroup) -- the count behind Table 2. */
+int attn_vgpr_estimate(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom,
+                       const attn_op_t* op, int t_q_wave, int t_kv, int n_waves,
+                       int32_t* out);
+
+/* Closed-formula tile derivation (Sections 4 and 5.4): LDS fixes t_kv, the
+ * register budget fixes t_q_wave, the CU count bounds the grid (splitting the
+ * key range, then shrinking the Q tile), and every tile is atom aligned.
+ * Returns ATTN_OK with report->feasible = 1, or ATTN_E_INFEASIBLE with
+ * report->binding naming the constraint that failed.  Host-only integer math. */
+int attn_tile_derive(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom,
+                     const attn_op_t* op, attn_tile_report_t* report);
+
+/* The report attn_fwd will act on for this shape: derivation over `hw`
+ * (NULL = query the current device) plus the compiled-instance check
+ * (ATTN_E_NO_INSTANCE if none matches). */
+int attn_fwd_plan(const attn_hw_desc_t* hw, int B, int H, int L, int d, int causal, int dtype,
+                  attn_tile_report_t* report);
+
+/* Fused attention forward (Algorithm 1 for every Q tile; Figure 2 mapping).
+ * scale: finite, >= 0 (1/sqrt(d) for standard attention).  causal != 0 keeps
+ * keys j <= i for query i (top-left aligned).  When the derivation splits the
+ * key range, partial results are merged with the Section 4.3 operator in a
+ * second kernel; the workspace for that is held by the library per device,
+ * grown on demand and kept until process exit (calls on one device that
+ * overlap in time on different streams must not share it: serialise them). */
+int attn_fwd(const void* Q, const void* K, const void* V, void* O,
+             int B, int H, int L, int d, float scale, int causal, int dtype, void* stream);
+
+/* Unfused baseline (Section 5.4, Table 3): three kernels on `stream` --
+ * S = scale Q K^T written to the workspace in `dtype`, a row softmax
+ * overwriting S with P (masked entries 0), then O = P V.  The workspace
+ * holds B*H*L*L elements; size it with attn_unfused_workspace_bytes. */
+int attn_fwd_unfused(const void* Q, const void* K, const void* V, void* O,
+                     int B, int H, int L, int d, float scale, int causal, int dtype,
+                     void* workspace, size_t workspace_bytes, void* stream);
+size_t attn_unfused_workspace_bytes(int B, int H, int L, int dtype);
+
+/* Matrix-core layout probe (Section 3.1: fragment ownership must be checked
+ * on the hardware).  Runs one 16x16x32 product with atom 0 = bf16, 1 = f16:
+ * A is a row-major 16 x 32 device array, Bm a row-major 32 x 16 array, C a
+ * row-major 16 x 16 float array written through the fragment layouts the
+ * attention kernel assumes.  C == A Bm iff those layouts are right. */
+int attn_mfma_probe(int atom, const void* A, const void* Bm, float* C, void* stream);
+
+const char* attn_strerror(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PAPER_2609_10937_ATTN_H */

@@ -1,0 +1,232 @@
+"""Python binding of libattn.so: the C ABI names, argument marshalling only.
+
+Every computation runs in the HIP library; this module converts torch
+tensors and Python values into pointers and integers and raises AttnError on
+a non-zero status.  Loading the library touches no GPU, so descriptor,
+derivation and argument-check entry points work on a host without one.
+If the library has not been built, load() raises; there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libattn.so")
+
+ATTN_BF16 = 0
+ATTN_F16 = 1
+ATTN_MAX_L = 1 << 24
+
+STATUS = {
+    0: "ATTN_OK", -1: "ATTN_E_NULLPTR", -2: "ATTN_E_SHAPE", -3: "ATTN_E_UNSUPPORTED_D",
+    -4: "ATTN_E_DTYPE", -5: "ATTN_E_ALIGN", -6: "ATTN_E_INFEASIBLE", -7: "ATTN_E_NO_INSTANCE",
+    -8: "ATTN_E_HIP", -9: "ATTN_E_WORKSPACE", -10: "ATTN_E_SCALE", -11: "ATTN_E_ARG",
+    -12: "ATTN_E_DEVICE",
+}
+CODE = {v: k for k, v in STATUS.items()}
+
+# Every function the header declares; the CPU tests check each is exported.
+EXPORTS = (
+    "attn_hw_desc_preset", "attn_hw_desc_query", "attn_atom_preset", "attn_fwd_op",
+    "attn_vgpr_estimate", "attn_tile_derive", "attn_fwd_plan", "attn_fwd", "attn_fwd_unfused",
+    "attn_unfused_workspace_bytes", "attn_mfma_probe", "attn_strerror",
+)
+
+c_int, c_int32, c_int64, c_float, c_double, c_char, c_size_t, c_void_p, c_char_p = (
+    ctypes.c_int, ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double,
+    ctypes.c_char, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_char_p)
+
+
+class _Struct(ctypes.Structure):
+    def as_dict(self):
+        out = {}
+        for name, _ in self._fields_:
+            v = getattr(self, name)
+            out[name] = v.decode() if isinstance(v, bytes) else v
+        return out
+
+
+class HwDesc(_Struct):
+    _fields_ = [("lds_bytes", c_int64), ("vgpr_per_thread", c_int32), ("wavefront_size", c_int32),
+                ("num_cus", c_int32), ("simds_per_cu", c_int32), ("lds_bytes_per_clk", c_int32),
+                ("mfma_flops_per_clk_cu", c_int32), ("hbm_tbps", c_double), ("peak_tflops", c_double),
+                ("clock_ghz", c_double), ("name", c_char * 32)]
+
+
+class Atom(_Struct):
+    _fields_ = [("m", c_int32), ("n", c_int32), ("k", c_int32), ("in_bytes", c_int32),
+                ("acc_bytes", c_int32)]
+
+
+class Op(_Struct):
+    _fields_ = [("B", c_int32), ("H", c_int32), ("L", c_int32), ("d", c_int32),
+                ("elem_bytes", c_int32), ("causal", c_int32), ("kv_lds_num", c_int32),
+                ("kv_lds_den", c_int32), ("kv_tiles", c_int32), ("stage_tiles", c_int32),
+                ("waves_per_wg", c_int32), ("waves_per_simd", c_int32), ("vgpr_fixed", c_int32),
+                ("max_split", c_int32)]
+
+
+class TileReport(_Struct):
+    _fields_ = [("feasible", c_int32), ("t_kv", c_int32), ("t_q_wave", c_int32),
+                ("n_waves", c_int32), ("tile_q", c_int32), ("n_split", c_int32),
+                ("grid", c_int64), ("vgpr_est", c_int32), ("vgpr_budget", c_int32),
+                ("lds_used", c_int64), ("lds_budget", c_int64), ("wg_per_cu", c_double),
+                ("low_occupancy", c_int32), ("lds_bw_ok", c_int32), ("binding", c_char * 16)]
+
+
+class AttnError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def load():
+    """Load libattn.so (no GPU access).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
+    lib = ctypes.CDLL(LIB_PATH)
+    P = ctypes.POINTER
+    sig = {
+        "attn_hw_desc_preset": (c_int, [c_char_p, P(HwDesc)]),
+        "attn_hw_desc_query": (c_int, [c_int, P(HwDesc)]),
+        "attn_atom_preset": (c_int, [c_char_p, P(Atom)]),
+        "attn_fwd_op": (c_int, [c_int, c_int, c_int, c_int, c_int, c_int, P(Op)]),
+        "attn_vgpr_estimate": (c_int, [P(HwDesc), P(Atom), P(Op), c_int, c_int, c_int, P(c_int32)]),
+        "attn_tile_derive": (c_int, [P(HwDesc), P(Atom), P(Op), P(TileReport)]),
+        "attn_fwd_plan": (c_int, [P(HwDesc), c_int, c_int, c_int, c_int, c_int, c_int, P(TileReport)]),
+        "attn_fwd": (c_int, [c_void_p, c_void_p, c_void_p, c_void_p, c_int, c_int, c_int, c_int,
+                             c_float, c_int, c_int, c_void_p]),
+        "attn_fwd_unfused": (c_int, [c_void_p, c_void_p, c_void_p, c_void_p, c_int, c_int, c_int,
+                                     c_int, c_float, c_int, c_int, c_void_p, c_size_t, c_void_p]),
+        "attn_unfused_workspace_bytes": (c_size_t, [c_int, c_int, c_int, c_int]),
+        "attn_mfma_probe": (c_int, [c_int, c_void_p, c_void_p, c_void_p, c_void_p]),
+        "attn_strerror": (c_char_p, [c_int]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(rc):
+    if rc != 0:
+        raise AttnError(rc, load().attn_strerror(rc).decode())
+    return rc
+
+
+# ------------------------------------------------------------ host-side calls
+
+def attn_hw_desc_preset(name: str) -> HwDesc:
+    d = HwDesc()
+    _check(load().attn_hw_desc_preset(name.encode(), ctypes.byref(d)))
+    return d
+
+
+def attn_hw_desc_query(device: int = 0) -> HwDesc:
+    d = HwDesc()
+    _check(load().attn_hw_desc_query(device, ctypes.byref(d)))
+    return d
+
+
+def attn_atom_preset(name: str) -> Atom:
+    a = Atom()
+    _check(load().attn_atom_preset(name.encode(), ctypes.byref(a)))
+    return a
+
+
+def attn_fwd_op(B, H, L, d, causal, dtype) -> Op:
+    o = Op()
+    _check(load().attn_fwd_op(B, H, L, d, int(causal), dtype, ctypes.byref(o)))
+    return o
+
+
+def attn_vgpr_estimate(hw: HwDesc, atom: Atom, op: Op, t_q_wave, t_kv, n_waves) -> int:
+    out = c_int32()
+    _check(load().attn_vgpr_estimate(ctypes.byref(hw), ctypes.byref(atom), ctypes.byref(op),
+                                     t_q_wave, t_kv, n_waves, ctypes.byref(out)))
+    return out.value
+
+
+def attn_tile_derive(hw: HwDesc, atom: Atom, op: Op):
+    """Returns (status, TileReport); ATTN_E_INFEASIBLE is a result, not an exception."""
+    r = TileReport()
+    rc = load().attn_tile_derive(ctypes.byref(hw), ctypes.byref(atom), ctypes.byref(op), ctypes.byref(r))
+    if rc not in (0, CODE["ATTN_E_INFEASIBLE"]):
+        _check(rc)
+    return rc, r
+
+
+def attn_fwd_plan(B, H, L, d, causal, dtype, hw: HwDesc | None = None) -> TileReport:
+    r = TileReport()
+    _check(load().attn_fwd_plan(ctypes.byref(hw) if hw is not None else None, B, H, L, d,
+                                int(causal), dtype, ctypes.byref(r)))
+    return r
+
+
+def attn_unfused_workspace_bytes(B, H, L, dtype) -> int:
+    return load().attn_unfused_workspace_bytes(B, H, L, dtype)
+
+
+def attn_strerror(status: int) -> str:
+    return load().attn_strerror(status).decode()
+
+
+# ------------------------------------------------------------ device calls
+
+def dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.bfloat16:
+        return ATTN_BF16
+    if t.dtype == torch.float16:
+        return ATTN_F16
+    raise AttnError(CODE["ATTN_E_DTYPE"], f"unsupported tensor dtype {t.dtype}")
+
+
+def _stream_ptr(t, stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream(t.device)
+    return c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _dev_ptr(t):
+    if not t.is_cuda:
+        raise AttnError(CODE["ATTN_E_ARG"], "tensor must be on the GPU")
+    if not t.is_contiguous():
+        raise AttnError(CODE["ATTN_E_ARG"], "tensor must be contiguous [B, H, L, d]")
+    return c_void_p(t.data_ptr())
+
+
+def attn_fwd(q, k, v, o, scale: float, causal: bool, stream=None):
+    """Enqueue the fused forward on `stream` (default: torch's current stream)."""
+    B, H, L, d = q.shape
+    for t in (k, v, o):
+        if tuple(t.shape) != (B, H, L, d) or t.dtype != q.dtype:
+            raise AttnError(CODE["ATTN_E_SHAPE"], "q, k, v, o must share shape and dtype")
+    _check(load().attn_fwd(_dev_ptr(q), _dev_ptr(k), _dev_ptr(v), _dev_ptr(o), B, H, L, d,
+                           float(scale), int(causal), dtype_code(q), _stream_ptr(q, stream)))
+
+
+def attn_fwd_unfused(q, k, v, o, scale: float, causal: bool, workspace, stream=None):
+    B, H, L, d = q.shape
+    for t in (k, v, o):
+        if tuple(t.shape) != (B, H, L, d) or t.dtype != q.dtype:
+            raise AttnError(CODE["ATTN_E_SHAPE"], "q, k, v, o must share shape and dtype")
+    nbytes = workspace.numel() * workspace.element_size()
+    _check(load().attn_fwd_unfused(_dev_ptr(q), _dev_ptr(k), _dev_ptr(v), _dev_ptr(o), B, H, L, d,
+                                   float(scale), int(causal), dtype_code(q), _dev_ptr(workspace),
+                                   nbytes, _stream_ptr(q, stream)))
+
+
+def attn_mfma_probe(atom: int, a, b, c, stream=None):
+    """a: [16, 32], b: [32, 16] (bf16 or f16 device tensors), c: [16, 16] float32 device tensor."""
+    _check(load().attn_mfma_probe(atom, _dev_ptr(a), _dev_ptr(b), _dev_ptr(c), _stream_ptr(a, stream)))

@@ -1,0 +1,354 @@
+// C ABI of the fused-attention library: argument checks, hardware
+// descriptors, tile derivation and dispatch to compiled kernel instances.
+#include <math.h>
+#include <string.h>
+
+#include <map>
+#include <mutex>
+#include <tuple>
+#include <vector>
+
+#include "internal.h"
+
+namespace attn {
+const FwdInstance* fwd_instances_bf16_d64(int* n);
+const FwdInstance* fwd_instances_bf16_d128(int* n);
+const FwdInstance* fwd_instances_f16_d64(int* n);
+const FwdInstance* fwd_instances_f16_d128(int* n);
+}  // namespace attn
+
+using namespace attn;
+
+namespace {
+
+// Fixed structure of the fused kernel family in fwd_kernel.hpp: K and V
+// double-buffered in half of LDS, the next tile staged through registers,
+// 8 waves per workgroup at 2 waves per SIMD.  vgpr_fixed is the compiled
+// register count of the (d=128, t_kv=64, 32 rows per wave, 8 waves)
+// instance minus the arrays the count names.
+constexpr int kKvLdsNum = 1, kKvLdsDen = 2, kKvTiles = 4, kStageTiles = 2;
+constexpr int kWavesPerWg = 8, kWavesPerSimd = 2, kVgprFixed = 107, kMaxSplit = 16;
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int check_shape(int B, int H, int L, int d, int dtype) {
+  if (B <= 0 || H <= 0 || L <= 0 || L > ATTN_MAX_L) return ATTN_E_SHAPE;
+  if (d != 64 && d != 128) return ATTN_E_UNSUPPORTED_D;
+  if (dtype != ATTN_BF16 && dtype != ATTN_F16) return ATTN_E_DTYPE;
+  const long double elems = (long double)B * H * L * d;
+  if (elems >= 4.6e18L) return ATTN_E_SHAPE;
+  if ((int64_t)B * H > (int64_t)1 << 30) return ATTN_E_SHAPE;
+  return ATTN_OK;
+}
+
+int check_tensors(const void* Q, const void* K, const void* V, const void* O) {
+  if (!Q || !K || !V || !O) return ATTN_E_NULLPTR;
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O)) return ATTN_E_ALIGN;
+  return ATTN_OK;
+}
+
+int check_scale(float scale) {
+  if (!isfinite(scale) || scale < 0.f) return ATTN_E_SCALE;
+  return ATTN_OK;
+}
+
+void fill_name(attn_hw_desc_t* d, const char* n) {
+  memset(d->name, 0, sizeof(d->name));
+  strncpy(d->name, n, sizeof(d->name) - 1);
+}
+
+void gfx950_desc(attn_hw_desc_t* d) {
+  memset(d, 0, sizeof(*d));
+  d->lds_bytes = 160 * 1024;
+  d->vgpr_per_thread = 512;       // 256 arch + 256 accumulation registers at one wave per SIMD
+  d->wavefront_size = 64;
+  d->num_cus = 256;
+  d->simds_per_cu = 4;
+  d->lds_bytes_per_clk = 128;
+  d->mfma_flops_per_clk_cu = 4096;  // dense bf16/fp16
+  d->hbm_tbps = 8.0;
+  d->peak_tflops = 2516.6;
+  d->clock_ghz = 2.4;
+  fill_name(d, "gfx950");
+}
+
+attn_mfma_atom_t atom_for(int dtype) {
+  (void)dtype;  // bf16 and f16 share the 16x16x32 shape and fp32 accumulation
+  attn_mfma_atom_t a = {16, 16, 32, 2, 4};
+  return a;
+}
+
+struct DeviceState {
+  bool have_desc = false;
+  attn_hw_desc_t desc{};
+  void* ws = nullptr;
+  size_t ws_bytes = 0;
+};
+
+std::mutex g_mu;
+std::map<int, DeviceState> g_dev;
+
+const FwdInstance* find_instance(int dtype, int d, int t_kv, int q_blocks, int n_waves) {
+  using Fn = const FwdInstance* (*)(int*);
+  Fn fns[] = {fwd_instances_bf16_d64, fwd_instances_bf16_d128, fwd_instances_f16_d64, fwd_instances_f16_d128};
+  for (Fn f : fns) {
+    int n = 0;
+    const FwdInstance* t = f(&n);
+    for (int i = 0; i < n; ++i)
+      if (t[i].dtype == dtype && t[i].d == d && t[i].t_kv == t_kv && t[i].q_blocks == q_blocks &&
+          t[i].n_waves == n_waves)
+        return &t[i];
+  }
+  return nullptr;
+}
+
+int query_desc(int device, attn_hw_desc_t* out) {
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, device) != hipSuccess) return ATTN_E_HIP;
+  if (strncmp(prop.gcnArchName, "gfx950", 6) != 0) return ATTN_E_DEVICE;
+  gfx950_desc(out);
+  out->num_cus = prop.multiProcessorCount;
+  out->lds_bytes = (int64_t)prop.sharedMemPerBlock;
+  out->wavefront_size = prop.warpSize;
+  if (prop.clockRate > 0) out->clock_ghz = prop.clockRate / 1e6;
+  out->peak_tflops = (double)out->mfma_flops_per_clk_cu * out->num_cus * out->clock_ghz / 1e3;
+  return ATTN_OK;
+}
+
+int device_desc(int device, attn_hw_desc_t* out) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  DeviceState& st = g_dev[device];
+  if (!st.have_desc) {
+    const int rc = query_desc(device, &st.desc);
+    if (rc != ATTN_OK) return rc;
+    st.have_desc = true;
+  }
+  *out = st.desc;
+  return ATTN_OK;
+}
+
+int make_op(int B, int H, int L, int d, int causal, int dtype, attn_op_t* op) {
+  memset(op, 0, sizeof(*op));
+  op->B = B;
+  op->H = H;
+  op->L = L;
+  op->d = d;
+  op->elem_bytes = 2;
+  op->causal = causal != 0;
+  op->kv_lds_num = kKvLdsNum;
+  op->kv_lds_den = kKvLdsDen;
+  op->kv_tiles = kKvTiles;
+  op->stage_tiles = kStageTiles;
+  op->waves_per_wg = kWavesPerWg;
+  op->waves_per_simd = kWavesPerSimd;
+  op->vgpr_fixed = kVgprFixed;
+  op->max_split = kMaxSplit;
+  (void)dtype;
+  return ATTN_OK;
+}
+
+int plan(const attn_hw_desc_t* hw, int B, int H, int L, int d, int causal, int dtype, attn_tile_report_t* rep,
+         const FwdInstance** inst) {
+  attn_op_t op;
+  make_op(B, H, L, d, causal, dtype, &op);
+  const attn_mfma_atom_t atom = atom_for(dtype);
+  const int rc = derive_tiles(hw, &atom, &op, rep);
+  if (rc != ATTN_OK) return rc;
+  if (rep->t_q_wave % 16) return ATTN_E_NO_INSTANCE;
+  const FwdInstance* f = find_instance(dtype, d, rep->t_kv, rep->t_q_wave / 16, rep->n_waves);
+  if (!f) return ATTN_E_NO_INSTANCE;
+  if (inst) *inst = f;
+  if (rep->grid > 0x7fffffffLL) return ATTN_E_SHAPE;
+  return ATTN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* attn_strerror(int status) {
+  switch (status) {
+    case ATTN_OK: return "ok";
+    case ATTN_E_NULLPTR: return "null pointer argument";
+    case ATTN_E_SHAPE: return "B, H or L out of range";
+    case ATTN_E_UNSUPPORTED_D: return "head dimension must be 64 or 128";
+    case ATTN_E_DTYPE: return "dtype must be ATTN_BF16 or ATTN_F16";
+    case ATTN_E_ALIGN: return "tensor base address not 16-byte aligned";
+    case ATTN_E_INFEASIBLE: return "tile derivation infeasible";
+    case ATTN_E_NO_INSTANCE: return "no compiled kernel for the derived tiles";
+    case ATTN_E_HIP: return "HIP runtime error";
+    case ATTN_E_WORKSPACE: return "workspace missing or too small";
+    case ATTN_E_SCALE: return "scale must be finite and >= 0";
+    case ATTN_E_ARG: return "invalid argument";
+    case ATTN_E_DEVICE: return "current device is not gfx950";
+    default: return "unknown status";
+  }
+}
+
+int attn_hw_desc_preset(const char* name, attn_hw_desc_t* out) {
+  if (!name || !out) return ATTN_E_NULLPTR;
+  if (strcmp(name, "gfx950") == 0) {
+    gfx950_desc(out);
+    return ATTN_OK;
+  }
+  const bool a = strcmp(name, "paper_gpu_a") == 0, b = strcmp(name, "paper_gpu_b") == 0;
+  if (!a && !b) return ATTN_E_ARG;
+  // Section 3, the two CDNA descriptors of the listing.
+  memset(out, 0, sizeof(*out));
+  out->lds_bytes = 64 * 1024;
+  out->vgpr_per_thread = 256;
+  out->wavefront_size = 64;
+  out->num_cus = a ? 120 : 304;
+  out->simds_per_cu = 4;
+  out->hbm_tbps = a ? 1.2 : 5.3;
+  out->peak_tflops = a ? 11.5 : 383.0;
+  fill_name(out, name);
+  return ATTN_OK;
+}
+
+int attn_hw_desc_query(int device, attn_hw_desc_t* out) {
+  if (!out) return ATTN_E_NULLPTR;
+  if (device < 0) return ATTN_E_ARG;
+  return device_desc(device, out);
+}
+
+int attn_atom_preset(const char* name, attn_mfma_atom_t* out) {
+  if (!name || !out) return ATTN_E_NULLPTR;
+  if (strcmp(name, "f32_16x16x4") == 0) {
+    *out = {16, 16, 4, 4, 4};
+    return ATTN_OK;
+  }
+  if (strcmp(name, "bf16_16x16x32") == 0 || strcmp(name, "f16_16x16x32") == 0) {
+    *out = {16, 16, 32, 2, 4};
+    return ATTN_OK;
+  }
+  return ATTN_E_ARG;
+}
+
+int attn_fwd_op(int B, int H, int L, int d, int causal, int dtype, attn_op_t* out) {
+  if (!out) return ATTN_E_NULLPTR;
+  const int rc = check_shape(B, H, L, d, dtype);
+  if (rc != ATTN_OK) return rc;
+  return make_op(B, H, L, d, causal, dtype, out);
+}
+
+int attn_vgpr_estimate(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const attn_op_t* op, int t_q_wave,
+                       int t_kv, int n_waves, int32_t* out) {
+  if (!hw || !atom || !op || !out) return ATTN_E_NULLPTR;
+  if (t_q_wave <= 0 || t_kv <= 0 || n_waves <= 0 || hw->wavefront_size <= 0 || atom->n <= 0) return ATTN_E_ARG;
+  *out = (int32_t)vgpr_estimate(hw, atom, op, t_q_wave, t_kv, n_waves);
+  return ATTN_OK;
+}
+
+int attn_tile_derive(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const attn_op_t* op,
+                     attn_tile_report_t* report) {
+  return derive_tiles(hw, atom, op, report);
+}
+
+int attn_fwd_plan(const attn_hw_desc_t* hw, int B, int H, int L, int d, int causal, int dtype,
+                  attn_tile_report_t* report) {
+  if (!report) return ATTN_E_NULLPTR;
+  int rc = check_shape(B, H, L, d, dtype);
+  if (rc != ATTN_OK) return rc;
+  attn_hw_desc_t desc;
+  if (!hw) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return ATTN_E_HIP;
+    rc = device_desc(dev, &desc);
+    if (rc != ATTN_OK) return rc;
+    hw = &desc;
+  }
+  return plan(hw, B, H, L, d, causal, dtype, report, nullptr);
+}
+
+int attn_fwd(const void* Q, const void* K, const void* V, void* O, int B, int H, int L, int d, float scale,
+             int causal, int dtype, void* stream) {
+  int rc = check_tensors(Q, K, V, O);
+  if (rc != ATTN_OK) return rc;
+  rc = check_shape(B, H, L, d, dtype);
+  if (rc != ATTN_OK) return rc;
+  rc = check_scale(scale);
+  if (rc != ATTN_OK) return rc;
+
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return ATTN_E_HIP;
+  attn_hw_desc_t desc;
+  rc = device_desc(dev, &desc);
+  if (rc != ATTN_OK) return rc;
+  attn_tile_report_t rep;
+  const FwdInstance* inst = nullptr;
+  rc = plan(&desc, B, H, L, d, causal, dtype, &rep, &inst);
+  if (rc != ATTN_OK) return rc;
+
+  FwdParams p{};
+  p.q = Q;
+  p.k = K;
+  p.v = V;
+  p.o = O;
+  p.BH = B * H;
+  p.L = L;
+  p.n_qt = (L + rep.tile_q - 1) / rep.tile_q;
+  p.n_split = rep.n_split;
+  const int n_kv = (L + rep.t_kv - 1) / rep.t_kv;
+  p.tiles_per_split = (n_kv + rep.n_split - 1) / rep.n_split;
+  p.causal = causal != 0;
+  p.c = scale * 1.4426950408889634f;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  if (p.n_split > 1) {
+    const size_t rows = (size_t)p.n_split * p.BH * L;
+    const size_t need = rows * (size_t)d * 4 + rows * 8;
+    std::lock_guard<std::mutex> lk(g_mu);
+    DeviceState& st = g_dev[dev];
+    if (st.ws_bytes < need) {
+      // Every earlier use of the old buffer was enqueued on some stream; wait
+      // for the device before releasing it.
+      if (st.ws) {
+        if (hipDeviceSynchronize() != hipSuccess) return ATTN_E_HIP;
+        (void)hipFree(st.ws);
+        st.ws = nullptr;
+        st.ws_bytes = 0;
+      }
+      if (hipMalloc(&st.ws, need) != hipSuccess) return ATTN_E_HIP;
+      st.ws_bytes = need;
+    }
+    p.part_o = static_cast<float*>(st.ws);
+    p.part_ml = reinterpret_cast<float*>(static_cast<char*>(st.ws) + rows * (size_t)d * 4);
+  }
+
+  if (inst->launch(p, (unsigned)rep.grid, s) != hipSuccess) return ATTN_E_HIP;
+  if (p.n_split > 1 && launch_combine(p, d, dtype, s) != hipSuccess) return ATTN_E_HIP;
+  return ATTN_OK;
+}
+
+size_t attn_unfused_workspace_bytes(int B, int H, int L, int dtype) {
+  if (B <= 0 || H <= 0 || L <= 0 || (dtype != ATTN_BF16 && dtype != ATTN_F16)) return 0;
+  return (size_t)B * H * (size_t)L * (size_t)L * 2;
+}
+
+int attn_fwd_unfused(const void* Q, const void* K, const void* V, void* O, int B, int H, int L, int d, float scale,
+                     int causal, int dtype, void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_tensors(Q, K, V, O);
+  if (rc != ATTN_OK) return rc;
+  rc = check_shape(B, H, L, d, dtype);
+  if (rc != ATTN_OK) return rc;
+  if (L % 8) return ATTN_E_SHAPE;  // 16-byte rows of the L x L matrix
+  rc = check_scale(scale);
+  if (rc != ATTN_OK) return rc;
+  if (!workspace) return ATTN_E_WORKSPACE;
+  if (!aligned16(workspace)) return ATTN_E_ALIGN;
+  if (workspace_bytes < attn_unfused_workspace_bytes(B, H, L, dtype)) return ATTN_E_WORKSPACE;
+  if ((int64_t)B * H > 65535 || (int64_t)B * H * L > 0x7fffffffLL) return ATTN_E_SHAPE;
+  const hipError_t e = launch_unfused(Q, K, V, O, workspace, B * H, L, d, scale, causal != 0, dtype,
+                                      static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? ATTN_OK : ATTN_E_HIP;
+}
+
+int attn_mfma_probe(int atom, const void* A, const void* Bm, float* C, void* stream) {
+  if (!A || !Bm || !C) return ATTN_E_NULLPTR;
+  if (atom != ATTN_BF16 && atom != ATTN_F16) return ATTN_E_ARG;
+  if (!aligned16(A)) return ATTN_E_ALIGN;
+  return launch_mfma_probe(atom, A, Bm, C, static_cast<hipStream_t>(stream)) == hipSuccess ? ATTN_OK : ATTN_E_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,55 @@
+// Internal declarations shared by the C-ABI layer and the HIP translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "attn.h"
+
+namespace attn {
+
+// Arguments of the fused kernel.  Tensor pointers are [B*H, L, d] contiguous.
+struct FwdParams {
+  const void* q;
+  const void* k;
+  const void* v;
+  void* o;
+  float* part_o;    // [n_split, BH, L, d] unnormalised partial outputs (n_split > 1)
+  float* part_ml;   // [n_split, BH, L, 2] running max (raw logit units) and sum
+  int BH;
+  int L;
+  int n_qt;             // query tiles per head
+  int n_split;          // key-range splits
+  int tiles_per_split;  // key tiles per split
+  int causal;
+  float c;              // scale * log2(e): exp(scale*(x - m)) = exp2(c*(x - m))
+};
+
+using FwdLaunch = hipError_t (*)(const FwdParams&, unsigned grid, hipStream_t);
+
+// One compiled instantiation of the fused kernel.
+struct FwdInstance {
+  int dtype;
+  int d;
+  int t_kv;
+  int q_blocks;   // query rows per wave / 16
+  int n_waves;
+  FwdLaunch launch;
+};
+
+const FwdInstance* fwd_instances(int* count);
+
+hipError_t launch_combine(const FwdParams& p, int d, int dtype, hipStream_t s);
+
+hipError_t launch_unfused(const void* q, const void* k, const void* v, void* o, void* ws,
+                          int BH, int L, int d, float scale, int causal, int dtype,
+                          hipStream_t s);
+
+hipError_t launch_mfma_probe(int atom, const void* a, const void* b, float* c, hipStream_t s);
+
+int derive_tiles(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const attn_op_t* op,
+                 attn_tile_report_t* rep);
+int64_t vgpr_estimate(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const attn_op_t* op,
+                      int64_t t_q, int64_t t_kv, int64_t n_w);
+
+}  // namespace attn

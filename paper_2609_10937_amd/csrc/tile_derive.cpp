@@ -1,0 +1,152 @@
+// Closed-formula tile derivation for the fused attention kernel.
+//
+// Sections 3-5 of the paper: tiles follow from three hardware constraints in
+// a CU-centric order, checked against the atom shape.
+//   1. LDS fixes the key/value tile: the staged tiles fill the LDS share the
+//      kernel structure gives them (Section 4, LDS constraint).
+//   2. The register budget fixes the query rows per wave, counting every array
+//      live at the synchronisation point between the two products: the Q
+//      operand, the fp32 score tile, the fp32 output accumulator and the
+//      running max/sum, plus staging registers and a fixed overhead
+//      (Section 5.4, Table 2 caption; Section 4, VGPR constraint).
+//   3. The CU count bounds the grid from below: split the key range (the
+//      merge of Section 4.3 is associative), then shrink the query tile
+//      (Section 4, occupancy constraint).
+//   4. Atom alignment (Section 4).
+// The count in step 2 is affine in t_q up to per-array register rounding, so
+// t_q is solved in closed form and then moved by at most a few atom steps to
+// absorb that rounding.
+#include <string.h>
+
+#include <algorithm>
+#include <numeric>
+
+#include "internal.h"
+
+namespace attn {
+
+static int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+int64_t vgpr_estimate(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const attn_op_t* op,
+                      int64_t t_q, int64_t t_kv, int64_t n_w) {
+  const int64_t lane_words = 4 * (int64_t)hw->wavefront_size;  // bytes in one register across a wave
+  const int64_t q_operand = cdiv(t_q * op->d * op->elem_bytes, lane_words);
+  const int64_t scores = cdiv(t_q * t_kv * atom->acc_bytes, lane_words);
+  const int64_t out_acc = cdiv(t_q * op->d * atom->acc_bytes, lane_words);
+  const int64_t stats = 2 * cdiv(t_q, atom->n);
+  const int64_t staging = cdiv((int64_t)op->stage_tiles * t_kv * op->d * op->elem_bytes, lane_words * n_w);
+  return q_operand + scores + out_acc + stats + staging + op->vgpr_fixed;
+}
+
+static void set_binding(attn_tile_report_t* r, const char* s) {
+  memset(r->binding, 0, sizeof(r->binding));
+  strncpy(r->binding, s, sizeof(r->binding) - 1);
+}
+
+int derive_tiles(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const attn_op_t* op,
+                 attn_tile_report_t* rep) {
+  if (!hw || !atom || !op || !rep) return ATTN_E_NULLPTR;
+  if (hw->lds_bytes <= 0 || hw->vgpr_per_thread <= 0 || hw->wavefront_size <= 0 ||
+      hw->num_cus <= 0 || hw->simds_per_cu <= 0)
+    return ATTN_E_ARG;
+  if (atom->m <= 0 || atom->n <= 0 || atom->k <= 0 || atom->in_bytes <= 0 || atom->acc_bytes <= 0)
+    return ATTN_E_ARG;
+  if (op->B <= 0 || op->H <= 0 || op->L <= 0 || op->d <= 0 || op->elem_bytes <= 0) return ATTN_E_ARG;
+  if (op->kv_lds_num <= 0 || op->kv_lds_den <= 0 || op->kv_tiles <= 0 || op->stage_tiles < 0 ||
+      op->waves_per_wg <= 0 || op->waves_per_simd <= 0 || op->vgpr_fixed < 0 || op->max_split < 1)
+    return ATTN_E_ARG;
+
+  memset(rep, 0, sizeof(*rep));
+  rep->n_split = 1;
+  rep->low_occupancy = 1;
+  rep->lds_bw_ok = 1;
+  const int64_t align_kv = std::lcm((int64_t)atom->n, (int64_t)atom->k);
+  const int64_t align_q = atom->n;
+  const int64_t lds_share = hw->lds_bytes * op->kv_lds_num / op->kv_lds_den;
+  const int64_t budget = hw->vgpr_per_thread / op->waves_per_simd;
+  rep->lds_budget = lds_share;
+  rep->vgpr_budget = (int32_t)budget;
+
+  // 4. The contraction over d (first product) and the d rows of the second
+  //    product must both be whole atoms.
+  if (op->d % atom->k || op->d % atom->m) {
+    set_binding(rep, "atom");
+    return ATTN_E_INFEASIBLE;
+  }
+
+  // 1. LDS -> t_kv.
+  int64_t t_kv = lds_share / ((int64_t)op->kv_tiles * op->d * op->elem_bytes);
+  t_kv -= t_kv % align_kv;
+  if (t_kv <= 0) {
+    set_binding(rep, "LDS");
+    return ATTN_E_INFEASIBLE;
+  }
+  rep->t_kv = (int32_t)t_kv;
+  rep->lds_used = (int64_t)op->kv_tiles * t_kv * op->d * op->elem_bytes;
+
+  // 2. Registers -> t_q per wave.  Without rounding the count is
+  //    t_q * slope + intercept with
+  //    slope = (d*elem + t_kv*acc + d*acc) / (4*wf) + 2/n.
+  int64_t n_w = op->waves_per_wg;
+  const double lw = 4.0 * hw->wavefront_size;
+  const double slope = ((double)op->d * op->elem_bytes + (double)t_kv * atom->acc_bytes +
+                        (double)op->d * atom->acc_bytes) / lw + 2.0 / atom->n;
+  const double intercept = (double)op->stage_tiles * t_kv * op->d * op->elem_bytes / (lw * n_w) +
+                           op->vgpr_fixed;
+  int64_t t_q = 0;
+  if (budget > intercept) {
+    t_q = (int64_t)((budget - intercept) / slope);
+    t_q -= t_q % align_q;
+  }
+  // Rounding of each array up to whole registers can only raise the count,
+  // by less than one register per term; step to the exact boundary.
+  while (t_q > 0 && vgpr_estimate(hw, atom, op, t_q, t_kv, n_w) > budget) t_q -= align_q;
+  while (vgpr_estimate(hw, atom, op, t_q + align_q, t_kv, n_w) <= budget) t_q += align_q;
+  if (t_q <= 0) {
+    set_binding(rep, "VGPR");
+    rep->vgpr_est = (int32_t)vgpr_estimate(hw, atom, op, align_q, t_kv, n_w);
+    return ATTN_E_INFEASIBLE;
+  }
+
+  // 3. CU count -> grid.
+  const char* binding = "VGPR";
+  const int64_t heads = (int64_t)op->B * op->H;
+  const int64_t n_kv = cdiv(op->L, t_kv);
+  int64_t n_qt = cdiv(op->L, n_w * t_q);
+  int64_t n_split = 1;
+  if (heads * n_qt < hw->num_cus && op->max_split > 1) {
+    const int64_t need = cdiv(hw->num_cus, heads * n_qt);
+    int64_t want = 1;
+    while (want < need) want *= 2;
+    n_split = std::min(std::min(want, (int64_t)op->max_split), n_kv);
+    n_split = cdiv(n_kv, cdiv(n_kv, n_split));  // no empty splits
+    if (n_split > 1) binding = "CU";
+  }
+  while (heads * n_qt * n_split < hw->num_cus) {
+    if (n_w > 1 && vgpr_estimate(hw, atom, op, t_q, t_kv, n_w / 2) <= budget)
+      n_w /= 2;
+    else if (t_q > align_q)
+      t_q -= align_q;
+    else
+      break;
+    n_qt = cdiv(op->L, n_w * t_q);
+    binding = "CU";
+  }
+
+  const int64_t grid = heads * n_qt * n_split;
+  rep->feasible = 1;
+  rep->t_q_wave = (int32_t)t_q;
+  rep->n_waves = (int32_t)n_w;
+  rep->tile_q = (int32_t)(n_w * t_q);
+  rep->n_split = (int32_t)n_split;
+  rep->grid = grid;
+  rep->vgpr_est = (int32_t)vgpr_estimate(hw, atom, op, t_q, t_kv, n_w);
+  rep->wg_per_cu = (double)grid / hw->num_cus;
+  rep->low_occupancy = grid < hw->num_cus;
+  if (hw->lds_bytes_per_clk > 0 && hw->mfma_flops_per_clk_cu > 0)
+    rep->lds_bw_ok = t_q * hw->lds_bytes_per_clk >= hw->mfma_flops_per_clk_cu;
+  set_binding(rep, binding);
+  return ATTN_OK;
+}
+
+}  // namespace attn

@@ -1,0 +1,230 @@
+"""Host-side tests of libattn.so: exports, argument checks, tile derivation.
+
+No GPU is touched: every argument check runs before the first HIP call, and
+the derivation is host integer arithmetic.  The C++ derivation is compared
+bit for bit with the oracle's model of the paper's rules (oracle/tile_model),
+which is itself pinned to Table 2.
+"""
+import ctypes
+import json
+import os
+import re
+
+import pytest
+from hypothesis import given, settings, strategies as stg
+
+from oracle import tile_model as T
+from paper_2609_10937_amd import capi, inputs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_every_declared_function_is_exported(lib):
+    with open(os.path.join(ROOT, "include", "attn.h")) as f:
+        header = f.read()
+    declared = set(re.findall(r"^(?:int|size_t|const char\*)\s+(attn_\w+)\(", header, re.M))
+    assert declared == set(capi.EXPORTS)
+    for name in declared:
+        assert hasattr(lib, name)
+
+
+def test_strerror_names_every_status(lib):
+    for code in capi.STATUS:
+        assert capi.attn_strerror(code) and capi.attn_strerror(code) != "unknown status"
+
+
+def test_presets():
+    g = capi.attn_hw_desc_preset("gfx950")
+    assert (g.lds_bytes, g.vgpr_per_thread, g.wavefront_size, g.num_cus) == (163840, 512, 64, 256)
+    a = capi.attn_hw_desc_preset("paper_gpu_a")
+    b = capi.attn_hw_desc_preset("paper_gpu_b")
+    assert (a.num_cus, b.num_cus, a.lds_bytes, a.vgpr_per_thread) == (120, 304, 65536, 256)
+    with pytest.raises(capi.AttnError) as e:
+        capi.attn_hw_desc_preset("gfx942")
+    assert e.value.status == capi.CODE["ATTN_E_ARG"]
+    at = capi.attn_atom_preset("f32_16x16x4")
+    assert (at.m, at.n, at.k, at.in_bytes, at.acc_bytes) == (16, 16, 4, 4, 4)
+
+
+def _to_c(hw, atom, op, st):
+    h = capi.HwDesc(lds_bytes=hw.lds_bytes, vgpr_per_thread=hw.vgpr_per_thread,
+                    wavefront_size=hw.wavefront_size, num_cus=hw.num_cus,
+                    simds_per_cu=hw.simds_per_cu, lds_bytes_per_clk=hw.lds_bytes_per_clk,
+                    mfma_flops_per_clk_cu=hw.mfma_flops_per_clk_cu)
+    a = capi.Atom(m=atom.m, n=atom.n, k=atom.k, in_bytes=atom.in_bytes, acc_bytes=atom.acc_bytes)
+    o = capi.Op(B=op.B, H=op.H, L=op.L, d=op.d, elem_bytes=op.elem_bytes, causal=int(op.causal),
+                kv_lds_num=st.kv_lds_num, kv_lds_den=st.kv_lds_den, kv_tiles=st.kv_tiles,
+                stage_tiles=st.stage_tiles, waves_per_wg=st.waves_per_wg,
+                waves_per_simd=st.waves_per_simd, vgpr_fixed=st.vgpr_fixed, max_split=st.max_split)
+    return h, a, o
+
+
+def _same(rc, rep, ref):
+    assert (rc == 0) == ref["feasible"]
+    assert rep.binding.decode() == ref["binding"]
+    if not ref["feasible"]:
+        return
+    for k in ("t_kv", "n_waves", "tile_q", "n_split", "grid", "vgpr_est", "vgpr_budget",
+              "lds_used", "lds_budget"):
+        assert getattr(rep, k) == ref[k], k
+    assert rep.t_q_wave == ref["t_q_wave"]
+    assert bool(rep.low_occupancy) == ref["low_occupancy"]
+    assert bool(rep.lds_bw_ok) == ref["lds_bw_ok"]
+    assert rep.wg_per_cu == pytest.approx(ref["wg_per_cu"], rel=1e-12)
+
+
+def test_table2_through_the_library():
+    with open(os.path.join(ROOT, "tests", "golden", "paper_tiles.json")) as f:
+        g = json.load(f)
+    hw = capi.attn_hw_desc_preset("paper_gpu_a")
+    atom = capi.attn_atom_preset("f32_16x16x4")
+    for r in g["table2"]:
+        op = capi.Op(B=1, H=1, L=16384, d=r["d"], elem_bytes=4, causal=0, kv_lds_num=1, kv_lds_den=2,
+                     kv_tiles=1, stage_tiles=0, waves_per_wg=1, waves_per_simd=1, vgpr_fixed=16,
+                     max_split=1)
+        rc, rep = capi.attn_tile_derive(hw, atom, op)
+        assert rc == 0 and rep.t_kv == r["t_kv"]
+        assert capi.attn_vgpr_estimate(hw, atom, op, r["t_q"], r["t_kv"], 1) == r["vgprs"]
+        if r["feasible"]:
+            assert rep.t_q_wave == r["t_q"] and rep.vgpr_est == r["vgprs"]
+    for name in ("paper_gpu_a", "paper_gpu_b"):
+        hw = capi.attn_hw_desc_preset(name)
+        rc, rep = capi.attn_tile_derive(hw, atom, op)
+        assert (rep.tile_q, rep.t_kv) == (g["portability"]["tile_q"], g["portability"]["tile_kv"])
+
+
+hw_s = stg.builds(T.Hardware,
+                  lds_bytes=stg.integers(1, 320).map(lambda x: x * 1024),
+                  vgpr_per_thread=stg.sampled_from([128, 256, 512]),
+                  wavefront_size=stg.sampled_from([32, 64]),
+                  num_cus=stg.integers(1, 512),
+                  simds_per_cu=stg.sampled_from([2, 4]),
+                  lds_bytes_per_clk=stg.sampled_from([0, 128, 256]),
+                  mfma_flops_per_clk_cu=stg.sampled_from([0, 2048, 4096]))
+atom_s = stg.sampled_from([T.Atom(16, 16, 4, 4, 4), T.Atom(16, 16, 32, 2, 4),
+                           T.Atom(32, 32, 16, 2, 4), T.Atom(16, 16, 16, 2, 4)])
+op_s = stg.builds(T.Op, B=stg.integers(1, 8), H=stg.integers(1, 64),
+                  L=stg.integers(1, 1 << 20), d=stg.sampled_from([16, 32, 48, 64, 96, 128, 256]),
+                  elem_bytes=stg.sampled_from([2, 4]), causal=stg.booleans())
+st_s = stg.builds(T.Structure, kv_lds_num=stg.just(1), kv_lds_den=stg.sampled_from([1, 2, 4]),
+                  kv_tiles=stg.sampled_from([1, 2, 4, 8]), stage_tiles=stg.sampled_from([0, 1, 2]),
+                  waves_per_wg=stg.sampled_from([1, 2, 4, 8, 16]),
+                  waves_per_simd=stg.sampled_from([1, 2, 4]),
+                  vgpr_fixed=stg.integers(0, 128), max_split=stg.sampled_from([1, 2, 8, 16]))
+
+
+@settings(max_examples=1500, deadline=None)
+@given(hw_s, atom_s, op_s, st_s)
+def test_library_derivation_matches_oracle_model(hw, atom, op, st):
+    ref = T.derive(hw, atom, op, st)
+    rc, rep = capi.attn_tile_derive(*_to_c(hw, atom, op, st))
+    _same(rc, rep, ref)
+
+
+def test_fused_structure_plans_every_shape():
+    """Every shape the API accepts maps to a compiled instance on the gfx950 descriptor."""
+    hw = capi.attn_hw_desc_preset("gfx950")
+    shapes = [(w.B, w.H, w.L, w.d, w.causal) for w in inputs.WORKLOADS.values()]
+    for d in (64, 128):
+        for L in (1, 2, 15, 16, 17, 31, 33, 63, 64, 65, 100, 127, 129, 159, 161, 1000, 1023, 4097,
+                  16384, 65536, 1 << 20, capi.ATTN_MAX_L):
+            for B, H in ((1, 1), (1, 3), (2, 8), (4, 32), (64, 64)):
+                for causal in (0, 1):
+                    shapes.append((B, H, L, d, causal))
+    seen = set()
+    for B, H, L, d, causal in shapes:
+        for dt in (capi.ATTN_BF16, capi.ATTN_F16):
+            if B * H * L > (1 << 31) // 2:
+                continue
+            r = capi.attn_fwd_plan(B, H, L, d, causal, dt, hw=hw)
+            assert r.feasible and r.grid >= 1
+            assert r.vgpr_est <= r.vgpr_budget and r.lds_used <= r.lds_budget
+            seen.add((d, r.t_kv, r.t_q_wave, r.n_waves))
+    assert (128, 64, 32, 8) in seen
+
+
+def test_headline_plans():
+    hw = capi.attn_hw_desc_preset("gfx950")
+    r = capi.attn_fwd_plan(1, 1, 16384, 128, 0, capi.ATTN_BF16, hw=hw)
+    assert (r.t_kv, r.t_q_wave, r.n_waves, r.tile_q) == (64, 32, 8, 256)
+    assert r.n_split == 4 and r.grid == 256 and r.binding == b"CU"
+    r = capi.attn_fwd_plan(4, 32, 16384, 128, 1, capi.ATTN_BF16, hw=hw)
+    assert (r.n_split, r.grid, r.binding) == (1, 8192, b"VGPR")
+
+
+# ------------------------------------------------------------ argument checks
+
+P = 1 << 20  # a 16-byte aligned fake device address; never dereferenced
+
+
+def _fwd(lib, q=P, k=P, v=P, o=P, B=1, H=1, L=16, d=64, scale=0.125, causal=0, dtype=0):
+    return lib.attn_fwd(q, k, v, o, B, H, L, d, scale, causal, dtype, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=None), "ATTN_E_NULLPTR"), (dict(o=None), "ATTN_E_NULLPTR"),
+    (dict(k=P + 8), "ATTN_E_ALIGN"), (dict(v=P + 2), "ATTN_E_ALIGN"),
+    (dict(B=0), "ATTN_E_SHAPE"), (dict(H=-1), "ATTN_E_SHAPE"), (dict(L=0), "ATTN_E_SHAPE"),
+    (dict(L=(1 << 24) + 1), "ATTN_E_SHAPE"), (dict(d=96), "ATTN_E_UNSUPPORTED_D"),
+    (dict(d=0), "ATTN_E_UNSUPPORTED_D"), (dict(dtype=2), "ATTN_E_DTYPE"),
+    (dict(scale=-1.0), "ATTN_E_SCALE"), (dict(scale=float("nan")), "ATTN_E_SCALE"),
+    (dict(scale=float("inf")), "ATTN_E_SCALE"),
+])
+def test_fwd_rejects_bad_arguments(lib, kw, code):
+    assert _fwd(lib, **kw) == capi.CODE[code]
+
+
+def test_unfused_rejects_bad_arguments(lib):
+    f = lib.attn_fwd_unfused
+    ws = capi.attn_unfused_workspace_bytes(1, 1, 16, 0)
+    assert ws == 16 * 16 * 2
+    assert f(P, P, P, P, 1, 1, 16, 64, 0.1, 0, 0, None, ws, None) == capi.CODE["ATTN_E_WORKSPACE"]
+    assert f(P, P, P, P, 1, 1, 16, 64, 0.1, 0, 0, P, ws - 1, None) == capi.CODE["ATTN_E_WORKSPACE"]
+    assert f(P, P, P, P, 1, 1, 16, 64, 0.1, 0, 0, P + 4, ws, None) == capi.CODE["ATTN_E_ALIGN"]
+    assert f(P, P, P, P, 1, 1, 12, 64, 0.1, 0, 0, P, ws, None) == capi.CODE["ATTN_E_SHAPE"]
+    assert f(None, P, P, P, 1, 1, 16, 64, 0.1, 0, 0, P, ws, None) == capi.CODE["ATTN_E_NULLPTR"]
+    assert capi.attn_unfused_workspace_bytes(0, 1, 16, 0) == 0
+
+
+def test_probe_rejects_bad_arguments(lib):
+    assert lib.attn_mfma_probe(0, None, P, P, None) == capi.CODE["ATTN_E_NULLPTR"]
+    assert lib.attn_mfma_probe(5, P, P, P, None) == capi.CODE["ATTN_E_ARG"]
+    assert lib.attn_mfma_probe(0, P + 8, P, P, None) == capi.CODE["ATTN_E_ALIGN"]
+
+
+def test_derive_rejects_bad_descriptors():
+    hw = capi.attn_hw_desc_preset("gfx950")
+    atom = capi.attn_atom_preset("bf16_16x16x32")
+    op = capi.attn_fwd_op(1, 1, 128, 64, 0, capi.ATTN_BF16)
+    bad = capi.HwDesc.from_buffer_copy(hw)
+    bad.num_cus = 0
+    with pytest.raises(capi.AttnError) as e:
+        capi.attn_tile_derive(bad, atom, op)
+    assert e.value.status == capi.CODE["ATTN_E_ARG"]
+    with pytest.raises(capi.AttnError):
+        capi.attn_fwd_op(1, 1, 128, 80, 0, capi.ATTN_BF16)
+
+
+# ------------------------------------------------------------ compiled resources
+
+def test_compiled_kernels_fit_without_scratch():
+    path = os.path.join(ROOT, "_build", "kernel_resources.json")
+    if not os.path.exists(path):
+        pytest.skip("resource report is written by the build")
+    with open(path) as f:
+        res = json.load(f)
+    fwd = {k: v for k, v in res.items() if "fwd_kernel" in k}
+    assert len(fwd) == 14
+    for name, r in res.items():
+        assert r["scratch"] == 0, name
+    for name, r in fwd.items():
+        nw = int(re.search(r"ILi\d+ELi\d+ELi\d+ELi\d+ELi(\d+)EE", name).group(1))
+        waves_per_simd = max(1, nw // 4)
+        assert r["vgpr"] + r["agpr"] <= 512 // waves_per_simd, name
+        assert r["lds"] <= 160 * 1024
+    # the design point the register count's fixed term was calibrated on
+    hw = capi.attn_hw_desc_preset("gfx950")
+    op = capi.attn_fwd_op(1, 1, 16384, 128, 0, capi.ATTN_BF16)
+    atom = capi.attn_atom_preset("bf16_16x16x32")
+    ref = [v for k, v in fwd.items() if "ILi0ELi128ELi64ELi2ELi8EE" in k][0]
+    assert ref["vgpr"] + ref["agpr"] <= capi.attn_vgpr_estimate(hw, atom, op, 32, 64, 8) <= 256

@@ -1,0 +1,191 @@
+"""GPU parity of the fused kernel (and the unfused baseline) with the CPU oracle.
+
+Every case prints its name before touching the GPU so a failure is
+attributable.  Inputs come from the seeded generator; expected values from
+oracle/ only.
+"""
+import numpy as np
+import pytest
+
+from oracle import attention as A
+from paper_2609_10937_amd import capi, inputs
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+import _gpu  # noqa: E402
+
+
+def _f64(bits, dtype):
+    return inputs.bits_to_f64(bits, dtype)
+
+
+# ------------------------------------------------------------ matrix-core layout
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+def test_mfma_fragment_layouts(dtype):
+    """Random small-integer operands: A B is exact in fp32, so C must match bit for bit."""
+    print(f"case mfma_probe {dtype}", flush=True)
+    rng = np.random.default_rng(5)
+    a = rng.integers(-8, 9, size=(16, 32)).astype(np.float32)
+    b = rng.integers(-8, 9, size=(32, 16)).astype(np.float32)
+    ta = _gpu.upload(inputs.round_bits(a, dtype), dtype)
+    tb = _gpu.upload(inputs.round_bits(b, dtype), dtype)
+    tc = torch.zeros((16, 16), dtype=torch.float32, device="cuda")
+    capi.attn_mfma_probe(0 if dtype == "bf16" else 1, ta, tb, tc)
+    torch.cuda.synchronize()
+    assert np.array_equal(tc.cpu().numpy(), a @ b)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+def test_paper_structured_layout_case(dtype):
+    """Section 3.1: Q[i,:] = i and K = I give C[i,:] = i; in the transposed
+    product the kernel uses (K Q^T) the same data gives C[:, j] = j."""
+    print(f"case mfma_structured {dtype}", flush=True)
+    q = np.repeat(np.arange(16, dtype=np.float32)[:, None], 32, axis=1)   # Q[i, :] = i
+    eye = np.zeros((16, 32), np.float32)
+    eye[:, :16] = np.eye(16)                                              # K = I (first 16 of d)
+    tc = torch.zeros((16, 16), dtype=torch.float32, device="cuda")
+    atom = 0 if dtype == "bf16" else 1
+    capi.attn_mfma_probe(atom, _gpu.upload(inputs.round_bits(q, dtype), dtype),
+                         _gpu.upload(inputs.round_bits(np.ascontiguousarray(eye.T), dtype), dtype), tc)
+    torch.cuda.synchronize()
+    assert np.array_equal(tc.cpu().numpy(), np.repeat(np.arange(16, dtype=np.float32)[:, None], 16, axis=1))
+    capi.attn_mfma_probe(atom, _gpu.upload(inputs.round_bits(eye, dtype), dtype),
+                         _gpu.upload(inputs.round_bits(np.ascontiguousarray(q.T), dtype), dtype), tc)
+    torch.cuda.synchronize()
+    assert np.array_equal(tc.cpu().numpy(), np.repeat(np.arange(16, dtype=np.float32)[None, :], 16, axis=0))
+
+
+# ------------------------------------------------------------ named workloads
+
+SMALL = ["tiny_f16_l128_d64", "h8_l1024_d128", "causal_b2h16_l4096_d128_kx3", "single_head_l16384_d128"]
+
+
+@pytest.mark.parametrize("name", SMALL)
+def test_workload_all_rows(name):
+    w = inputs.WORKLOADS[name]
+    print(f"case workload {name}", flush=True)
+    q, k, v = inputs.workload_inputs(w)
+    o = _gpu.fused(_gpu.upload(q, w.dtype), _gpu.upload(k, w.dtype), _gpu.upload(v, w.dtype), w.scale, w.causal)
+    got = _gpu.download(o, w.dtype)
+    ref = A.attention(_f64(q, w.dtype), _f64(k, w.dtype), _f64(v, w.dtype), w.scale, w.causal)
+    mx, mn = _gpu.assert_close(got, ref, w.dtype, name)
+    floor = np.abs(_f64(inputs.round_bits(ref.astype(np.float32), w.dtype), w.dtype) - ref).max()
+    print(f"  {name}: max_abs {mx:.3e} mean_abs {mn:.3e} (rounding floor {floor:.3e})", flush=True)
+
+
+def test_full_occupancy_causal_sampled_rows():
+    """B=4, H=32, L=16384 causal: sampled heads and rows against the oracle,
+    plus properties that hold for every row (finite, inside the range of V)."""
+    w = inputs.WORKLOADS["causal_b4h32_l16384_d128"]
+    print(f"case workload {w.name} (sampled)", flush=True)
+    q, k, v = inputs.workload_inputs(w)
+    tq, tk, tv = (_gpu.upload(x, w.dtype) for x in (q, k, v))
+    o = _gpu.fused(tq, tk, tv, w.scale, w.causal)
+    rng = np.random.default_rng(77)
+    L = w.L
+    for b, h in ((0, 0), (1, 17), (3, 31), (2, 5)):
+        rows = np.unique(np.concatenate([np.arange(0, 40), np.arange(L - 40, L),
+                                         rng.integers(0, L, 120), [255, 256, 257, 8191, 8192]]))
+        got = _gpu.download(o[b, h, torch.from_numpy(rows).to("cuda")], w.dtype)
+        ref = A.attention_head(_f64(q[b, h], w.dtype), _f64(k[b, h], w.dtype), _f64(v[b, h], w.dtype),
+                               w.scale, True, rows=rows)
+        _gpu.assert_close(got, ref, w.dtype, f"{w.name} b{b} h{h}")
+    of = o.float()
+    assert torch.isfinite(of).all()
+    vf = tv.float()
+    # causal row i is a convex combination of V[0..i]: bounded by the running min/max
+    vmax = torch.cummax(vf, dim=2).values
+    vmin = -torch.cummax(-vf, dim=2).values
+    slack = 2e-2
+    assert (of <= vmax + slack).all() and (of >= vmin - slack).all()
+
+
+# ------------------------------------------------------------ edge shapes
+
+EDGE = [(L, d, causal, dt) for L in (1, 17, 100, 1000, 4097) for d in (64, 128)
+        for causal in (False, True) for dt in ("bf16", "f16")]
+
+
+@pytest.mark.parametrize("L,d,causal,dtype", EDGE)
+def test_edge_shapes(L, d, causal, dtype):
+    B, H = (2, 3) if L <= 1000 else (1, 2)
+    print(f"case edge L{L} d{d} causal{int(causal)} {dtype}", flush=True)
+    q, k, v = inputs.make_qkv(B, H, L, d, dtype, seed=L * 7 + d, k_scale=2.0)
+    scale = inputs.softmax_scale(d)
+    o = _gpu.fused(_gpu.upload(q, dtype), _gpu.upload(k, dtype), _gpu.upload(v, dtype), scale, causal)
+    ref = A.attention(_f64(q, dtype), _f64(k, dtype), _f64(v, dtype), scale, causal)
+    _gpu.assert_close(_gpu.download(o, dtype), ref, dtype, f"L{L} d{d} c{causal} {dtype}")
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_many_heads_small_l(causal):
+    """B*H large enough that the grid covers the CUs without splitting."""
+    print(f"case many_heads causal{int(causal)}", flush=True)
+    q, k, v = inputs.make_qkv(8, 40, 200, 128, "bf16", seed=91)
+    s = inputs.softmax_scale(128)
+    o = _gpu.fused(_gpu.upload(q, "bf16"), _gpu.upload(k, "bf16"), _gpu.upload(v, "bf16"), s, causal)
+    ref = A.attention(_f64(q, "bf16"), _f64(k, "bf16"), _f64(v, "bf16"), s, causal)
+    _gpu.assert_close(_gpu.download(o, "bf16"), ref, "bf16", "many heads")
+
+
+# ------------------------------------------------------------ invariants on the GPU
+
+def test_gpu_invariants():
+    print("case invariants", flush=True)
+    B, H, L, d = 1, 2, 700, 128
+    q, k, v = inputs.make_qkv(B, H, L, d, "bf16", seed=123)
+    s = inputs.softmax_scale(d)
+    tq, tk, tv = (_gpu.upload(x, "bf16") for x in (q, k, v))
+    # constant V -> O equals that constant exactly (weights sum to one in fp32)
+    vc = tv.clone()
+    vc[:] = tv[:, :, :1, :]
+    for causal in (False, True):
+        o = _gpu.fused(tq, tk, vc, s, causal)
+        assert torch.equal(o, vc), "constant V"
+    # causal row 0 is V[0] exactly
+    o = _gpu.fused(tq, tk, tv, s, True)
+    assert torch.equal(o[:, :, 0], tv[:, :, 0])
+    # Q = 0 (or scale 0) -> column means of V (prefix means when causal)
+    vf = _f64(v, "bf16")
+    mean = vf.mean(axis=2, keepdims=True)
+    prefix = np.cumsum(vf, axis=2) / np.arange(1, L + 1)[None, None, :, None]
+    for zq, sc in ((True, s), (False, 0.0)):
+        qq = torch.zeros_like(tq) if zq else tq
+        o = _gpu.download(_gpu.fused(qq, tk, tv, sc, False), "bf16")
+        _gpu.assert_close(o, np.broadcast_to(mean, o.shape), "bf16", "uniform weights")
+        oc = _gpu.download(_gpu.fused(qq, tk, tv, sc, True), "bf16")
+        _gpu.assert_close(oc, prefix, "bf16", "uniform causal weights")
+
+
+def test_bitwise_deterministic():
+    print("case determinism", flush=True)
+    w = inputs.WORKLOADS["single_head_l16384_d128"]
+    q, k, v = (_gpu.upload(x, w.dtype) for x in inputs.workload_inputs(w))
+    a = _gpu.fused(q, k, v, w.scale, w.causal)
+    b = _gpu.fused(q, k, v, w.scale, w.causal)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+# ------------------------------------------------------------ unfused baseline
+
+@pytest.mark.parametrize("L,causal", [(1024, False), (256, True)])
+def test_unfused_baseline(L, causal):
+    """Scores and probabilities are stored in bf16 between the kernels, so the
+    baseline is held to a looser bound than the fused kernel (it is a
+    reference for time and traffic, not for accuracy)."""
+    print(f"case unfused L{L} causal{int(causal)}", flush=True)
+    B, H, d = 1, 8, 128
+    q, k, v = inputs.make_qkv(B, H, L, d, "bf16", seed=1002)
+    s = inputs.softmax_scale(d)
+    tq, tk, tv = (_gpu.upload(x, "bf16") for x in (q, k, v))
+    o = torch.empty_like(tq)
+    ws = torch.empty(capi.attn_unfused_workspace_bytes(B, H, L, capi.ATTN_BF16), dtype=torch.uint8, device="cuda")
+    capi.attn_fwd_unfused(tq, tk, tv, o, s, causal, ws)
+    torch.cuda.synchronize()
+    got = _gpu.download(o, "bf16")
+    ref = A.attention(_f64(q, "bf16"), _f64(k, "bf16"), _f64(v, "bf16"), s, causal)
+    mx, mn = _gpu.errors(got, ref)
+    print(f"  unfused max_abs {mx:.3e} mean_abs {mn:.3e}", flush=True)
+    assert np.all(np.isfinite(got)) and mx <= 6e-2 and mn <= 6e-3
