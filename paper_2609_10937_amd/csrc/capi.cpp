@@ -21,13 +21,14 @@ using namespace attn;
 
 namespace {
 
-// Fixed structure of the fused kernel family in fwd_kernel.hpp: K and V
-// double-buffered in half of LDS, the next tile staged through registers,
-// 8 waves per workgroup at 2 waves per SIMD.  vgpr_fixed is the compiled
-// register count of the (d=128, t_kv=64, 32 rows per wave, 8 waves)
-// instance minus the arrays the count names.
-constexpr int kKvLdsNum = 1, kKvLdsDen = 2, kKvTiles = 4, kStageTiles = 2;
-constexpr int kWavesPerWg = 8, kWavesPerSimd = 2, kVgprFixed = 107, kMaxSplit = 16;
+// Fixed structure of the fused kernel family in fwd_kernel.hpp: all of LDS
+// holds a ring of 5 stages of (K tile, V tile) filled by direct HBM->LDS
+// copies (no registers stage them), 8 waves per workgroup at 2 waves per
+// SIMD.  vgpr_fixed is the compiled register count of the (d=128, t_kv=64,
+// 32 rows per wave, 8 waves) instance minus the arrays the count names
+// (200 - 132): operand fragments in flight, addresses, loop state.
+constexpr int kKvLdsNum = 1, kKvLdsDen = 1, kKvTiles = 10, kStageTiles = 0;
+constexpr int kWavesPerWg = 8, kWavesPerSimd = 2, kVgprFixed = 68, kMaxSplit = 16;
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 

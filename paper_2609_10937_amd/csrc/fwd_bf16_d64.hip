@@ -1,15 +1,18 @@
-// Fused-kernel instantiations for dtype bf16, head dimension 64 (t_kv = 160):
-// every (query blocks per wave, waves per workgroup) the tile derivation can
-// reach for this head dimension on a gfx950 descriptor.
+// Fused-kernel instantiations for dtype bf16, head dimension 64 (t_kv = 128,
+// 5 LDS stages): every (query blocks per wave, waves per workgroup) the tile
+// derivation can reach for this head dimension on a gfx950 descriptor.
 #include "fwd_kernel.hpp"
 
 namespace attn {
 
 const FwdInstance* fwd_instances_bf16_d64(int* n) {
   static const FwdInstance table[] = {
-      {ATTN_BF16, 64, 160, 1, 8, launch_fwd<ATTN_BF16, 64, 160, 1, 8>},
-      {ATTN_BF16, 64, 160, 1, 4, launch_fwd<ATTN_BF16, 64, 160, 1, 4>},
-      {ATTN_BF16, 64, 160, 1, 2, launch_fwd<ATTN_BF16, 64, 160, 1, 2>},
+      {ATTN_BF16, 64, 128, 3, 8, launch_fwd<ATTN_BF16, 64, 128, 3, 8, 5>},
+      {ATTN_BF16, 64, 128, 3, 4, launch_fwd<ATTN_BF16, 64, 128, 3, 4, 5>},
+      {ATTN_BF16, 64, 128, 3, 2, launch_fwd<ATTN_BF16, 64, 128, 3, 2, 5>},
+      {ATTN_BF16, 64, 128, 3, 1, launch_fwd<ATTN_BF16, 64, 128, 3, 1, 5>},
+      {ATTN_BF16, 64, 128, 2, 1, launch_fwd<ATTN_BF16, 64, 128, 2, 1, 5>},
+      {ATTN_BF16, 64, 128, 1, 1, launch_fwd<ATTN_BF16, 64, 128, 1, 1, 5>},
   };
   *n = (int)(sizeof(table) / sizeof(table[0]));
   return table;

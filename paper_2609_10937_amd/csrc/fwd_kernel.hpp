@@ -5,26 +5,42 @@
 // tiles of its workgroup's range:
 //   GEMM1  S^T = K_t Q^T          (v_mfma_f32_16x16x32_{bf16,f16}, fp32 acc)
 //   mask   causal / past-the-end keys -> -inf (Section 4.3 padding rule)
-//   stats  running max m and sum delta per query row (online softmax)
+//   stats  running reference max m and sum delta per query row
 //   GEMM2  O^T = V_t^T P^T        (same atom, fp32 acc)
 // Computing S transposed puts query q on lane%16 in both products: the C
 // fragment of S^T (lane holds S^T[4*(lane/16)+r][lane%16]) is, after packing
 // to 16 bits, exactly the B operand of the second product once its k index is
-// permuted (k = 8*(lane/16)+e  <->  key 4*(lane/16)+e or 16+4*(lane/16)+e-4);
-// V^T is read from LDS with the same permutation.  So P never leaves
-// registers -- the paper's E_t^T LDS round trip (Section 5.3) is gone.
+// permuted (k = 8*(lane/16)+e  <->  key 4*(lane/16)+e or 16+4*(lane/16)+e-4).
+// V^T is read with the same permutation by the transposing LDS read.  So P
+// never leaves registers -- the paper's E_t^T LDS round trip (Section 5.3)
+// is gone.
 //
-// Fragment layouts (Section 3.1 warns they are a hardware fact, not a
-// consequence of the shape; attn_mfma_probe checks them on the device):
+// Fragment layouts (Section 3.1: a hardware fact, checked on the device by
+// attn_mfma_probe):
 //   A[16 x 32]: lane holds A[lane%16][8*(lane/16) + 0..7]
 //   B[32 x 16]: lane holds B[8*(lane/16) + 0..7][lane%16]
 //   C[16 x 16]: lane holds C[4*(lane/16) + 0..3][lane%16]
+// ds_read_b64_tr_b16, within each 16-lane group: lane i receives element i%4
+// of the 4-element rows addressed by lanes 4e+i/4, e = 0..3.  Pointing lane j
+// at V[row0 + j/4][col0 + 4*(j%4)] therefore hands lane i the column
+// V[row0 .. row0+3][col0 + i]: four keys of one output column, the A operand.
 //
-// LDS holds two buffers of {K tile row-major [t_kv][d], V tile transposed
-// [d][t_kv]}.  16-byte K chunks are XOR-swizzled by row and 8-byte V^T
-// granules by d so that the operand reads of one wave hit distinct banks.
-// The next tile is loaded from HBM into registers while the current one is
-// computed (one barrier per tile).
+// LDS holds a ring of ST stages, each a K tile and a V tile stored row-major
+// ([t_kv][d]) in 16-byte chunks, XOR-swizzled per row so that the operand
+// reads of a 16-lane group touch distinct banks.  Tiles move HBM -> LDS with
+// global_load_lds_dwordx4 (lane l of a wave writes bytes 16l..16l+15 of a
+// 1 KB block; each lane picks the source chunk that belongs at its slot), so
+// no registers stage them and nothing is transposed on the way.  Up to
+// ST-2 tiles beyond the one being computed are in flight; one barrier per
+// tile.
+//
+// Softmax bookkeeping keeps a per-row reference max m that is only raised
+// when a new row maximum exceeds it by more than 2^TAU in the exponent (the
+// merge of Section 4.3 holds for any common reference point, so the result is
+// the same; exponentiated weights stay below 2^TAU).  Most tiles then need no
+// rescaling of O.  The row sum adds the 16-bit weights that enter the second
+// product (v_dot2 with ones), so the weights the output is normalised by are
+// exactly the ones applied to V.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -35,10 +51,17 @@
 namespace attn {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef short i16x8_t __attribute__((ext_vector_type(8)));
+
+#define ATTN_LDS __attribute__((address_space(3)))
+#define ATTN_GLOBAL __attribute__((address_space(1)))
 
 template <int DT>
 struct Mfma;
@@ -46,18 +69,29 @@ struct Mfma;
 template <>
 struct Mfma<ATTN_BF16> {
   using V8 = bf16x8_t;
+  using V2 = bf16x2_t;
   using S = __bf16;
   static __device__ __forceinline__ f32x4_t run(V8 a, V8 b, f32x4_t c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+  // a.x + a.y (+ acc), exact products with one, fp32 accumulation
+  static __device__ __forceinline__ float sum2(V2 a, float acc) {
+    const V2 one = {(__bf16)1.0f, (__bf16)1.0f};
+    return __builtin_amdgcn_fdot2_f32_bf16(a, one, acc, false);
   }
 };
 
 template <>
 struct Mfma<ATTN_F16> {
   using V8 = f16x8_t;
+  using V2 = f16x2_t;
   using S = _Float16;
   static __device__ __forceinline__ f32x4_t run(V8 a, V8 b, f32x4_t c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ float sum2(V2 a, float acc) {
+    const V2 one = {(_Float16)1.0f, (_Float16)1.0f};
+    return __builtin_amdgcn_fdot2(a, one, acc, false);
   }
 };
 
@@ -67,37 +101,50 @@ __device__ __forceinline__ u32x4_t ldg16(const uint16_t* p) {
 
 __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// XOR swizzle of the 8-byte granule index of a V^T row (granules per row = G).
-template <int G>
-__device__ __forceinline__ int vt_swizzle(int d) {
-  if constexpr (G % 16 == 0)
-    return d & 15;
-  else
-    return (d >> 1) & 7;
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
+// vmcnt[3:0] in bits 3:0, vmcnt[5:4] in bits 15:14; expcnt and lgkmcnt at max).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
-template <int DT, int D, int TKV, int QB, int NW>
+// Workgroup barrier that orders LDS accesses but leaves in-flight
+// global->LDS copies alone (the compiler's __syncthreads would drain them).
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// 16-byte chunk swizzles of a row-major [rows][KCH chunks] tile.
+template <int KCH>
+__device__ __forceinline__ int k_swz(int r) { return r & (KCH - 1); }
+__device__ __forceinline__ int v_swz(int r) { return 2 * (r & 3); }
+
+template <int DT, int D, int TKV, int QB, int NW, int ST>
 __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   using M = Mfma<DT>;
   using V8 = typename M::V8;
+  using V2 = typename M::V2;
   using S = typename M::S;
-  constexpr int NT = NW * 64;
-  constexpr int TQW = 16 * QB;          // query rows per wave
-  constexpr int TILE_Q = NW * TQW;      // query rows per workgroup
-  constexpr int KC = D / 32;            // k steps of GEMM1
-  constexpr int NKB = TKV / 16;         // 16-key blocks of S^T
-  constexpr int NP = TKV / 32;          // k steps of GEMM2
-  constexpr int NDB = D / 16;           // 16-row blocks of O^T
-  constexpr int KCH = D / 8;            // 16-byte chunks per K row
-  constexpr int K_CHUNKS = TKV * KCH;
-  constexpr int K_PT = (K_CHUNKS + NT - 1) / NT;
-  constexpr int VG = TKV / 4;           // 8-byte granules per V^T row
-  constexpr int V_UNITS = VG * (D / 8); // 4 keys x 8 columns per unit
-  constexpr int V_PT = (V_UNITS + NT - 1) / NT;
-  constexpr int TILE = TKV * D;
-  static_assert(TKV % 32 == 0 && D % 32 == 0 && (KCH & (KCH - 1)) == 0, "tile alignment");
+  constexpr int TQW = 16 * QB;              // query rows per wave
+  constexpr int TILE_Q = NW * TQW;          // query rows per workgroup
+  constexpr int KC = D / 32;                // k steps of GEMM1
+  constexpr int NKB = TKV / 16;             // 16-key blocks of S^T
+  constexpr int NP = TKV / 32;              // k steps of GEMM2
+  constexpr int NDB = D / 16;               // 16-row blocks of O^T
+  constexpr int KCH = D / 8;                // 16-byte chunks per row
+  constexpr int TILE = TKV * D;             // elements of one K or V tile
+  constexpr int CHUNKS = TKV * KCH;
+  constexpr int LPW = CHUNKS / (NW * 64);   // 1 KB copies per wave per tile and tensor
+  constexpr float TAU = 8.0f;
+  static_assert(TKV % 32 == 0 && D % 32 == 0 && KCH >= 8 && (KCH & (KCH - 1)) == 0, "tile alignment");
+  static_assert(CHUNKS % (NW * 64) == 0, "tile copies must split evenly across waves");
+  // Tiles kept in flight beyond the one being computed: bounded by the ring
+  // (ST - 2) and by the 6-bit vector-memory counter (2*LPW copies per tile).
+  constexpr int DEPTH = (ST - 2) < 63 / (2 * LPW) ? (ST - 2) : 63 / (2 * LPW);
+  static_assert(ST >= 2 && DEPTH >= 0, "stages");
 
-  __shared__ __attribute__((aligned(16))) uint16_t smem[4 * TILE];
+  __shared__ __attribute__((aligned(1024))) uint16_t smem[ST * 2 * TILE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -131,6 +178,27 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   const int t_begin = split * p.tiles_per_split;
   const int t_end = min(n_kv, t_begin + p.tiles_per_split);
 
+  // Copy tile t of K and V into stage `stage`: the wave's LPW 1 KB blocks of
+  // each tile image.  Image slot P holds row P/KCH, logical chunk
+  // (P%KCH) ^ swizzle(row).  Rows past the end are clamped to row L-1
+  // (finite data that the mask removes).
+  auto issue = [&](int t, int stage) {
+    const int kv0 = t * TKV;
+    uint16_t* ks = smem + stage * 2 * TILE;
+    uint16_t* vs = ks + TILE;
+#pragma unroll
+    for (int i = 0; i < LPW; ++i) {
+      const int blk = w * LPW + i;
+      const int P = blk * 64 + lane;
+      const int r = P / KCH, pc = P % KCH;
+      const size_t row = (size_t)min(kv0 + r, L - 1) * D;
+      __builtin_amdgcn_global_load_lds((ATTN_GLOBAL void*)(Kh + row + ((pc ^ k_swz<KCH>(r)) * 8)),
+                                       (ATTN_LDS void*)(ks + blk * 512), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((ATTN_GLOBAL void*)(Vh + row + ((pc ^ v_swz(r)) * 8)),
+                                       (ATTN_LDS void*)(vs + blk * 512), 16, 0, 0);
+    }
+  };
+
   // Q fragments: B operand of S^T = K Q^T, one 16-byte load per (block, k step).
   V8 qf[QB][KC];
 #pragma unroll
@@ -143,6 +211,11 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
       qf[qb][kc] = __builtin_bit_cast(V8, x);
     }
   }
+  // Drain the Q loads here: the loop's waits count only tile copies.
+  wait_vmcnt<0>();
+#pragma unroll
+  for (int j = 0; j <= DEPTH; ++j)
+    if (t_begin + j < t_end) issue(t_begin + j, j);
 
   f32x4_t o[QB][NDB];
   float m[QB], l[QB];
@@ -154,87 +227,30 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
     for (int db = 0; db < NDB; ++db) o[qb][db] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
   }
 
-  u32x4_t kst[K_PT];
-  u32x4_t vst[V_PT][4];
-
-  auto gload = [&](int t) {
-    const int kv0 = t * TKV;
-#pragma unroll
-    for (int i = 0; i < K_PT; ++i) {
-      const int ci = tid + i * NT;
-      u32x4_t x = {0u, 0u, 0u, 0u};
-      if (K_CHUNKS % NT == 0 || ci < K_CHUNKS) {
-        const int r = ci / KCH, cc = ci % KCH;
-        if (kv0 + r < L) x = ldg16(Kh + (size_t)(kv0 + r) * D + cc * 8);
-      }
-      kst[i] = x;
-    }
-#pragma unroll
-    for (int i = 0; i < V_PT; ++i) {
-      const int ui = tid + i * NT;
-      const int kq = ui % VG, dc = ui / VG;
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        u32x4_t x = {0u, 0u, 0u, 0u};
-        const int kv = kv0 + 4 * kq + rr;
-        if ((V_UNITS % NT == 0 || ui < V_UNITS) && kv < L) x = ldg16(Vh + (size_t)kv * D + dc * 8);
-        vst[i][rr] = x;
-      }
-    }
-  };
-
-  auto lstore = [&](int buf) {
-    uint16_t* Ks = smem + buf * 2 * TILE;
-    uint16_t* Vt = Ks + TILE;
-#pragma unroll
-    for (int i = 0; i < K_PT; ++i) {
-      const int ci = tid + i * NT;
-      if (K_CHUNKS % NT == 0 || ci < K_CHUNKS) {
-        const int r = ci / KCH, cc = ci % KCH;
-        const int phys = cc ^ (r & (KCH - 1));
-        *reinterpret_cast<u32x4_t*>(Ks + r * D + phys * 8) = kst[i];
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < V_PT; ++i) {
-      const int ui = tid + i * NT;
-      if (V_UNITS % NT == 0 || ui < V_UNITS) {
-        const int kq = ui % VG, dc = ui / VG;
-        // vst[i][rr] = V[kv0 + 4kq + rr][8dc .. 8dc+7]; write column e of these
-        // four rows as one 8-byte granule of V^T row 8dc+e.
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int j = e >> 1;
-          uint32_t lo, hi;
-          if (e & 1) {
-            lo = (vst[i][0][j] >> 16) | (vst[i][1][j] & 0xffff0000u);
-            hi = (vst[i][2][j] >> 16) | (vst[i][3][j] & 0xffff0000u);
-          } else {
-            lo = (vst[i][0][j] & 0xffffu) | (vst[i][1][j] << 16);
-            hi = (vst[i][2][j] & 0xffffu) | (vst[i][3][j] << 16);
-          }
-          const int d = 8 * dc + e;
-          const int phys = kq ^ vt_swizzle<VG>(d);
-          *reinterpret_cast<u32x2_t*>(Vt + d * TKV + phys * 4) = (u32x2_t){lo, hi};
-        }
-      }
-    }
-  };
-
   const float cs = p.c;
-  if (t_begin < t_end) gload(t_begin);
-  int buf = 0;
+  const float thr = TAU / cs;  // +inf when cs == 0: the reference never moves
+  int stage = 0;
   for (int t = t_begin; t < t_end; ++t) {
-    lstore(buf);
-    __syncthreads();
-    if (t + 1 < t_end) gload(t + 1);
+    // This wave's copies of tile t are complete once no more than the copies
+    // of the tiles issued after it (up to DEPTH tiles) are outstanding;
+    // vector-memory operations retire in issue order.
+    const int after = min(DEPTH, t_end - 1 - t);
+    if (after >= DEPTH) wait_vmcnt<2 * LPW * DEPTH>();
+    else if (after == 2) wait_vmcnt<(DEPTH > 2 ? 4 * LPW : 0)>();
+    else if (after == 1) wait_vmcnt<(DEPTH > 1 ? 2 * LPW : 0)>();
+    else wait_vmcnt<0>();
+    lds_barrier();  // tile t visible to all waves; every wave is done with tile t-1
+    if (t + DEPTH + 1 < t_end) {
+      const int st_next = stage + DEPTH + 1 >= ST ? stage + DEPTH + 1 - ST : stage + DEPTH + 1;
+      issue(t + DEPTH + 1, st_next);
+    }
 
     const int kv0 = t * TKV;
     // Wave-uniform: skip waves with no valid row or whose rows all precede the tile.
     const bool live = (q0 < L) && !(p.causal && kv0 > q0 + TQW - 1);
     if (live) {
-      const uint16_t* Ks = smem + buf * 2 * TILE;
-      const uint16_t* Vt = Ks + TILE;
+      const uint16_t* Ks = smem + stage * 2 * TILE;
+      const uint16_t* Vs = Ks + TILE;
       const bool need_mask = (kv0 + TKV > L) || (p.causal && kv0 + TKV - 1 > q0);
 
       // GEMM1: s[kb][qb][r] = <K[kv0 + 16kb + 4g + r], Q[q0 + 16qb + c]>
@@ -246,7 +262,7 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
         const int row = 16 * kb + c;
 #pragma unroll
         for (int kc = 0; kc < KC; ++kc) {
-          const int phys = (4 * kc + g) ^ (row & (KCH - 1));
+          const int phys = (4 * kc + g) ^ k_swz<KCH>(row);
           const V8 kf = __builtin_bit_cast(V8, *reinterpret_cast<const u32x4_t*>(Ks + row * D + phys * 8));
 #pragma unroll
           for (int qb = 0; qb < QB; ++qb) s[kb][qb] = M::run(kf, qf[qb][kc], s[kb][qb]);
@@ -269,16 +285,22 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
         float mx = -INFINITY;
 #pragma unroll
         for (int kb = 0; kb < NKB; ++kb)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) mx = fmaxf(mx, s[kb][qb][r]);
+          mx = fmaxf(mx, fmaxf(fmaxf(s[kb][qb][0], s[kb][qb][1]), fmaxf(s[kb][qb][2], s[kb][qb][3])));
         mx = fmaxf(mx, __shfl_xor(mx, 16));
         mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m[qb], mx);
-        // A row that has seen only masked keys keeps reference 0 (no exp(-inf+inf)).
-        const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-        const float corr = (m[qb] == -INFINITY) ? 0.f : exp2_hw((m[qb] - m_use) * cs);
-        const float mc = m_use * cs;
-        float rs = 0.f;
+        // Raise the reference only when the exponent would exceed TAU (and on
+        // a row's first visible key, whatever the scale).
+        const float lim = (m[qb] == -INFINITY) ? -INFINITY : m[qb] + thr;
+        if (__any(mx > lim)) {
+          const float m_new = fmaxf(m[qb], mx);
+          const float corr = (m[qb] == -INFINITY) ? 0.f : exp2_hw((m[qb] - m_new) * cs);
+          l[qb] *= corr;
+#pragma unroll
+          for (int db = 0; db < NDB; ++db) o[qb][db] *= corr;
+          m[qb] = m_new;
+        }
+        const float mc = (m[qb] == -INFINITY) ? 0.f : m[qb] * cs;
+        float rs = l[qb];
 #pragma unroll
         for (int pp = 0; pp < NP; ++pp) {
           S e8[8];
@@ -290,33 +312,42 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
               float e = exp2_hw(__builtin_fmaf(x, cs, -mc));
               if (need_mask && x == -INFINITY) e = 0.f;
               e8[4 * h + r] = (S)e;
-              rs += (float)e8[4 * h + r];  // the sum uses the rounded weights
             }
-          pk[pp][qb] = (V8){e8[0], e8[1], e8[2], e8[3], e8[4], e8[5], e8[6], e8[7]};
+          const V8 pv = (V8){e8[0], e8[1], e8[2], e8[3], e8[4], e8[5], e8[6], e8[7]};
+          rs = M::sum2((V2){pv[0], pv[1]}, rs);
+          rs = M::sum2((V2){pv[2], pv[3]}, rs);
+          rs = M::sum2((V2){pv[4], pv[5]}, rs);
+          rs = M::sum2((V2){pv[6], pv[7]}, rs);
+          pk[pp][qb] = pv;
         }
-        l[qb] = l[qb] * corr + rs;
-        m[qb] = m_new;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) o[qb][db] *= corr;
+        l[qb] = rs;
       }
 
       // GEMM2: o[qb][db][r] += sum_k V^T[16db + 4g + r][k] P^T[k][q]
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
-        const int d = 16 * db + c;
-        const int sw = vt_swizzle<VG>(d);
-        const uint16_t* vrow = Vt + d * TKV;
+        // lane c addresses row 4g + c/4 (+16 for the upper half), column 16db + 4(c%4)
+        const int col = 16 * db + 4 * (c & 3);
+        const int cpart = 4 * (c & 1);
 #pragma unroll
         for (int pp = 0; pp < NP; ++pp) {
-          const u32x2_t a0 = *reinterpret_cast<const u32x2_t*>(vrow + (((8 * pp + g) ^ sw) * 4));
-          const u32x2_t a1 = *reinterpret_cast<const u32x2_t*>(vrow + (((8 * pp + 4 + g) ^ sw) * 4));
-          const V8 vf = __builtin_bit_cast(V8, (u32x4_t){a0.x, a0.y, a1.x, a1.y});
+          i16x4_t half[2];
 #pragma unroll
-          for (int qb = 0; qb < QB; ++qb) o[qb][db] = M::run(vf, pk[pp][qb], o[qb][db]);
+          for (int h = 0; h < 2; ++h) {
+            const int R = 32 * pp + 16 * h + 4 * g + (c >> 2);
+            const int phys = (col >> 3) ^ v_swz(R);
+            half[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (ATTN_LDS i16x4_t*)(Vs + R * D + phys * 8 + cpart));
+          }
+          const i16x8_t cat = {half[0][0], half[0][1], half[0][2], half[0][3],
+                               half[1][0], half[1][1], half[1][2], half[1][3]};
+          const V8 va = __builtin_bit_cast(V8, cat);
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb) o[qb][db] = M::run(va, pk[pp][qb], o[qb][db]);
         }
       }
     }
-    buf ^= 1;
+    stage = (stage + 1 == ST) ? 0 : stage + 1;
   }
 
   // Epilogue.  Each of the four lane groups holds a partial row sum over its
@@ -351,9 +382,9 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   }
 }
 
-template <int DT, int D, int TKV, int QB, int NW>
+template <int DT, int D, int TKV, int QB, int NW, int ST>
 hipError_t launch_fwd(const FwdParams& p, unsigned grid, hipStream_t s) {
-  hipLaunchKernelGGL((fwd_kernel<DT, D, TKV, QB, NW>), dim3(grid), dim3(NW * 64), 0, s, p);
+  hipLaunchKernelGGL((fwd_kernel<DT, D, TKV, QB, NW, ST>), dim3(grid), dim3(NW * 64), 0, s, p);
   return hipGetLastError();
 }
 
