@@ -38,7 +38,10 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", os.path.
           "-I", HERE, "-Wall", "-Wno-unused-function"]
 # Packed fp32 VALU forms are kept out of the device code.
 DEVICE = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-          "-Rpass-analysis=kernel-resource-usage"]
+          "-Rpass-analysis=kernel-resource-usage",
+          # No NaN operands are relied on (infinities are): max/min need no
+          # NaN-quieting canonicalisation.
+          "-fno-honor-nans"]
 
 
 def _hipcc():

@@ -24,11 +24,13 @@ namespace {
 // Fixed structure of the fused kernel family in fwd_kernel.hpp: all of LDS
 // holds a ring of 5 stages of (K tile, V tile) filled by direct HBM->LDS
 // copies (no registers stage them), 8 waves per workgroup at 2 waves per
-// SIMD.  vgpr_fixed is the compiled register count of the (d=128, t_kv=64,
-// 32 rows per wave, 8 waves) instance minus the arrays the count names
-// (200 - 132): operand fragments in flight, addresses, loop state.
+// SIMD.  vgpr_fixed covers what the count does not name (operand fragments
+// in flight, addresses, loop state, mask bookkeeping): the smallest value for
+// which every tile the derivation accepts compiles without spilling (the
+// d=64, 48-rows-per-wave kernel needs more than 256 registers, which a
+// fixed term of 83 or more excludes).
 constexpr int kKvLdsNum = 1, kKvLdsDen = 1, kKvTiles = 10, kStageTiles = 0;
-constexpr int kWavesPerWg = 8, kWavesPerSimd = 2, kVgprFixed = 68, kMaxSplit = 16;
+constexpr int kWavesPerWg = 8, kWavesPerSimd = 2, kVgprFixed = 83, kMaxSplit = 16;
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 

@@ -7,10 +7,9 @@ namespace attn {
 
 const FwdInstance* fwd_instances_f16_d64(int* n) {
   static const FwdInstance table[] = {
-      {ATTN_F16, 64, 128, 3, 8, launch_fwd<ATTN_F16, 64, 128, 3, 8, 5>},
-      {ATTN_F16, 64, 128, 3, 4, launch_fwd<ATTN_F16, 64, 128, 3, 4, 5>},
-      {ATTN_F16, 64, 128, 3, 2, launch_fwd<ATTN_F16, 64, 128, 3, 2, 5>},
-      {ATTN_F16, 64, 128, 3, 1, launch_fwd<ATTN_F16, 64, 128, 3, 1, 5>},
+      {ATTN_F16, 64, 128, 2, 8, launch_fwd<ATTN_F16, 64, 128, 2, 8, 5>},
+      {ATTN_F16, 64, 128, 2, 4, launch_fwd<ATTN_F16, 64, 128, 2, 4, 5>},
+      {ATTN_F16, 64, 128, 2, 2, launch_fwd<ATTN_F16, 64, 128, 2, 2, 5>},
       {ATTN_F16, 64, 128, 2, 1, launch_fwd<ATTN_F16, 64, 128, 2, 1, 5>},
       {ATTN_F16, 64, 128, 1, 1, launch_fwd<ATTN_F16, 64, 128, 1, 1, 5>},
   };

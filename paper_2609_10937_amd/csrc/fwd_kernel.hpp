@@ -101,6 +101,26 @@ __device__ __forceinline__ u32x4_t ldg16(const uint16_t* p) {
 
 __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Maximum over the four 16-lane rows of a wave (lanes l, l^16, l^32, l^48),
+// with the row-swapping permutes of CDNA4 (VALU, no LDS round trip).
+__device__ __forceinline__ float max_across_rows(float x) {
+  const uint32_t u = __builtin_bit_cast(uint32_t, x);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const float y = fmaxf(__builtin_bit_cast(float, (uint32_t)a[0]), __builtin_bit_cast(float, (uint32_t)a[1]));
+  const uint32_t v = __builtin_bit_cast(uint32_t, y);
+  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return fmaxf(__builtin_bit_cast(float, (uint32_t)b[0]), __builtin_bit_cast(float, (uint32_t)b[1]));
+}
+
+__device__ __forceinline__ float sum_across_rows(float x) {
+  const uint32_t u = __builtin_bit_cast(uint32_t, x);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const float y = __builtin_bit_cast(float, (uint32_t)a[0]) + __builtin_bit_cast(float, (uint32_t)a[1]);
+  const uint32_t v = __builtin_bit_cast(uint32_t, y);
+  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return __builtin_bit_cast(float, (uint32_t)b[0]) + __builtin_bit_cast(float, (uint32_t)b[1]);
+}
+
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
 // vmcnt[3:0] in bits 3:0, vmcnt[5:4] in bits 15:14; expcnt and lgkmcnt at max).
 template <int N>
@@ -119,6 +139,74 @@ __device__ __forceinline__ void lds_barrier() {
 template <int KCH>
 __device__ __forceinline__ int k_swz(int r) { return r & (KCH - 1); }
 __device__ __forceinline__ int v_swz(int r) { return 2 * (r & 3); }
+
+// Online-softmax step of Algorithm 1 for one tile of scores s (S^T
+// fragments, raw logits): row maxima, the lazily raised reference max, the
+// 16-bit weights packed as the B operand of the second product, and the row
+// sums of those weights.  MASK = true for tiles crossing the causal diagonal
+// or the end of the sequence.
+template <bool MASK, typename M, int NKB, int NP, int QB, int NDB>
+__device__ __forceinline__ void softmax_tile(f32x4_t (&s)[NKB][QB], typename M::V8 (&pk)[NP][QB], float (&m)[QB],
+                                             float (&l)[QB], f32x4_t (&o)[QB][NDB], int kv0, int q0, int g, int c,
+                                             int L, int causal, float cs, float thr) {
+  using V2 = typename M::V2;
+  using S = typename M::S;
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int q = q0 + 16 * qb + c;
+    bool keep[NKB][4];
+    if constexpr (MASK) {
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int kv = kv0 + 16 * kb + 4 * g + r;
+          keep[kb][r] = kv < L && !(causal && kv > q);
+          if (!keep[kb][r]) s[kb][qb][r] = -INFINITY;
+        }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb)
+      mx = fmaxf(fmaxf(mx, s[kb][qb][0]), fmaxf(fmaxf(s[kb][qb][1], s[kb][qb][2]), s[kb][qb][3]));
+    mx = max_across_rows(mx);
+    // Raise the reference only when an exponent would exceed TAU (and on a
+    // row's first visible key, whatever the scale).
+    const float lim = (m[qb] == -INFINITY) ? -INFINITY : m[qb] + thr;
+    if (__any(mx > lim)) {
+      const float m_new = fmaxf(m[qb], mx);
+      const float corr = (m[qb] == -INFINITY) ? 0.f : exp2_hw((m[qb] - m_new) * cs);
+      l[qb] *= corr;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) o[qb][db] *= corr;
+      m[qb] = m_new;
+    }
+    const float mc = (m[qb] == -INFINITY) ? 0.f : m[qb] * cs;
+    float rs = l[qb];
+#pragma unroll
+    for (int pp = 0; pp < NP; ++pp) {
+      V2 h2[4];
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int r = 0; r < 4; r += 2) {
+          float e0 = exp2_hw(__builtin_fmaf(s[2 * pp + h][qb][r], cs, -mc));
+          float e1 = exp2_hw(__builtin_fmaf(s[2 * pp + h][qb][r + 1], cs, -mc));
+          if constexpr (MASK) {
+            e0 = keep[2 * pp + h][r] ? e0 : 0.f;
+            e1 = keep[2 * pp + h][r + 1] ? e1 : 0.f;
+          }
+          h2[2 * h + r / 2] = (V2){(S)e0, (S)e1};
+        }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) rs = M::sum2(h2[j], rs);
+      pk[pp][qb] = __builtin_shufflevector(__builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3),
+                                           __builtin_shufflevector(h2[2], h2[3], 0, 1, 2, 3),
+                                           0, 1, 2, 3, 4, 5, 6, 7);
+    }
+    l[qb] = rs;
+  }
+}
 
 template <int DT, int D, int TKV, int QB, int NW, int ST>
 __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
@@ -270,58 +358,10 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
       }
 
       V8 pk[NP][QB];
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        if (need_mask) {
-          const int q = q0 + 16 * qb + c;
-#pragma unroll
-          for (int kb = 0; kb < NKB; ++kb)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const int kv = kv0 + 16 * kb + 4 * g + r;
-              if (kv >= L || (p.causal && kv > q)) s[kb][qb][r] = -INFINITY;
-            }
-        }
-        float mx = -INFINITY;
-#pragma unroll
-        for (int kb = 0; kb < NKB; ++kb)
-          mx = fmaxf(mx, fmaxf(fmaxf(s[kb][qb][0], s[kb][qb][1]), fmaxf(s[kb][qb][2], s[kb][qb][3])));
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        // Raise the reference only when the exponent would exceed TAU (and on
-        // a row's first visible key, whatever the scale).
-        const float lim = (m[qb] == -INFINITY) ? -INFINITY : m[qb] + thr;
-        if (__any(mx > lim)) {
-          const float m_new = fmaxf(m[qb], mx);
-          const float corr = (m[qb] == -INFINITY) ? 0.f : exp2_hw((m[qb] - m_new) * cs);
-          l[qb] *= corr;
-#pragma unroll
-          for (int db = 0; db < NDB; ++db) o[qb][db] *= corr;
-          m[qb] = m_new;
-        }
-        const float mc = (m[qb] == -INFINITY) ? 0.f : m[qb] * cs;
-        float rs = l[qb];
-#pragma unroll
-        for (int pp = 0; pp < NP; ++pp) {
-          S e8[8];
-#pragma unroll
-          for (int h = 0; h < 2; ++h)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const float x = s[2 * pp + h][qb][r];
-              float e = exp2_hw(__builtin_fmaf(x, cs, -mc));
-              if (need_mask && x == -INFINITY) e = 0.f;
-              e8[4 * h + r] = (S)e;
-            }
-          const V8 pv = (V8){e8[0], e8[1], e8[2], e8[3], e8[4], e8[5], e8[6], e8[7]};
-          rs = M::sum2((V2){pv[0], pv[1]}, rs);
-          rs = M::sum2((V2){pv[2], pv[3]}, rs);
-          rs = M::sum2((V2){pv[4], pv[5]}, rs);
-          rs = M::sum2((V2){pv[6], pv[7]}, rs);
-          pk[pp][qb] = pv;
-        }
-        l[qb] = rs;
-      }
+      if (need_mask)
+        softmax_tile<true, M>(s, pk, m, l, o, kv0, q0, g, c, L, p.causal, cs, thr);
+      else
+        softmax_tile<false, M>(s, pk, m, l, o, kv0, q0, g, c, L, p.causal, cs, thr);
 
       // GEMM2: o[qb][db][r] += sum_k V^T[16db + 4g + r][k] P^T[k][q]
 #pragma unroll
@@ -354,8 +394,7 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   // key subset (same reference max), so the total is their sum.
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
-    float lt = l[qb] + __shfl_xor(l[qb], 16);
-    lt += __shfl_xor(lt, 32);
+    const float lt = sum_across_rows(l[qb]);
     const int q = q0 + 16 * qb + c;
     if (p.n_split == 1) {
       const float inv = lt > 0.f ? 1.f / lt : 0.f;

@@ -214,7 +214,7 @@ def test_compiled_kernels_fit_without_scratch():
     with open(path) as f:
         res = json.load(f)
     fwd = {k: v for k, v in res.items() if "fwd_kernel" in k}
-    assert len(fwd) == 22
+    assert len(fwd) == 20
     for name, r in res.items():
         assert r["scratch"] == 0, name
     for name, r in fwd.items():
@@ -227,4 +227,6 @@ def test_compiled_kernels_fit_without_scratch():
     op = capi.attn_fwd_op(1, 1, 16384, 128, 0, capi.ATTN_BF16)
     atom = capi.attn_atom_preset("bf16_16x16x32")
     ref = [v for k, v in fwd.items() if "ILi0ELi128ELi64ELi2ELi8ELi5EE" in k][0]
-    assert ref["vgpr"] + ref["agpr"] == capi.attn_vgpr_estimate(hw, atom, op, 32, 64, 8) <= 256
+    assert ref["vgpr"] + ref["agpr"] <= capi.attn_vgpr_estimate(hw, atom, op, 32, 64, 8) <= 256
+    # one more query block per wave is refused by the count (and would spill)
+    assert capi.attn_vgpr_estimate(hw, atom, op, 48, 64, 8) > 256
