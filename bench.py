@@ -99,6 +99,33 @@ def cpu_baseline(w, q, k, v):
                       f"(B=1, H=1, d={w.d}), {dt:.2f} s"}
 
 
+def kernel_source_hash():
+    """Hash of the fused kernel's sources: a traffic figure measured on other sources is stale."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_10937_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.startswith("fwd_") or name == "internal.h":
+            with open(os.path.join(csrc, name), "rb") as f:
+                h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload):
+    """HBM bytes per fused-kernel launch from the committed counter summary, if it
+    was taken on the current kernel sources (else None)."""
+    path = os.path.join(ROOT, "profiles", "fwd_kernel_traffic.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    entry = rec.get("workloads", {}).get(workload)
+    return None if entry is None else entry.get("hbm_bytes_per_launch")
+
+
 def sampled_parity(w, q, k, v, out):
     from oracle import attention as A
     import torch
@@ -119,6 +146,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle timing")
     ap.add_argument("--no-secondary", action="store_true", help="skip the batched causal workload")
+    ap.add_argument("--no-unfused", action="store_true", help="skip the unfused baseline")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="finish with two plain 256 MiB device copies (reference for byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -143,20 +173,33 @@ def main():
     wall_ms, ev_ms = time_steps(step, args.steps, args.warmup)
     fl = flops(w)
     value = fl / (wall_ms * 1e-3) / 1e12
-    achieved = fl / (ev_ms * 1e-3) / 1e12
     parity = sampled_parity(w, q, k, v, to)
 
-    print("bench: unfused", file=sys.stderr, flush=True)
-    ws = torch.empty(capi.attn_unfused_workspace_bytes(w.B, w.H, w.L, capi.ATTN_BF16), dtype=torch.uint8,
-                     device="cuda")
-    tu = torch.empty_like(tq)
+    # The dominant kernel on its own: attn_fwd_partial launches exactly the
+    # fused kernel (the split merge, when there is one, is attn_fwd_merge).
+    ws_bytes = capi.attn_fwd_workspace_bytes(w.B, w.H, w.L, w.d, w.causal, capi.ATTN_BF16)
+    ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device="cuda") if ws_bytes else None
 
-    def ustep():
-        capi.attn_fwd_unfused(tq, tk, tv, tu, w.scale, w.causal, ws)
+    def kstep():
+        capi.attn_fwd_partial(tq, tk, tv, to, w.scale, w.causal, ws)
 
-    u_wall, u_ev = time_steps(ustep, max(3, args.steps // 2), 2)
+    _, k_ms = time_steps(kstep, args.steps, args.warmup)
+    achieved = fl / (k_ms * 1e-3) / 1e12
     del ws
-    torch.cuda.empty_cache()
+
+    u_ev = None
+    if not args.no_unfused:
+        print("bench: unfused", file=sys.stderr, flush=True)
+        ws = torch.empty(capi.attn_unfused_workspace_bytes(w.B, w.H, w.L, capi.ATTN_BF16), dtype=torch.uint8,
+                         device="cuda")
+        tu = torch.empty_like(tq)
+
+        def ustep():
+            capi.attn_fwd_unfused(tq, tk, tv, tu, w.scale, w.causal, ws)
+
+        _, u_ev = time_steps(ustep, max(3, args.steps // 2), 2)
+        del ws
+        torch.cuda.empty_cache()
 
     secondary = None
     if not args.no_secondary:
@@ -203,18 +246,29 @@ def main():
                               "clock_ghz": desc.clock_ghz}},
         "pct_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 5), "traffic": None,
-                     "kernel": "fused attention step (fwd_kernel + split merge), HIP events per step",
-                     "event_ms": round(ev_ms, 5)},
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 5),
+                     "traffic": measured_traffic(w.name),
+                     "kernel": "fwd_kernel (attn_fwd_partial), HIP events per launch",
+                     "kernel_ms": round(k_ms, 5), "step_event_ms": round(ev_ms, 5),
+                     "algorithmic_flops_per_launch": fl, "algorithmic_bytes_per_launch": fused_bytes(w)},
         "hbm_bytes": {"fused_algorithmic": fused_bytes(w), "unfused_algorithmic": unfused_bytes(w),
                       "ratio": unfused_bytes(w) / fused_bytes(w)},
-        "unfused": {"ms": round(u_ev, 4), "tflops": round(fl / (u_ev * 1e-3) / 1e12, 2),
-                    "speedup_fused_over_unfused": round(u_ev / ev_ms, 3),
-                    "hbm_rate_tbps": round(unfused_bytes(w) / (u_ev * 1e-3) / 1e12, 3)},
+        "unfused": None if u_ev is None else {
+            "ms": round(u_ev, 4), "tflops": round(fl / (u_ev * 1e-3) / 1e12, 2),
+            "speedup_fused_over_unfused": round(u_ev / ev_ms, 3),
+            "algorithmic_bytes": unfused_bytes(w),
+            "hbm_rate_tbps": round(unfused_bytes(w) / (u_ev * 1e-3) / 1e12, 3)},
         "parity": parity,
         "secondary": secondary,
         "cpu_baseline": cpu,
     }
+    if args.copy_calibration:
+        src = torch.ones(64 << 20, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     print(json.dumps(out), flush=True)
 
 

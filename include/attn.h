@@ -86,6 +86,7 @@ typedef struct {
   int32_t kv_lds_num, kv_lds_den; /* share of LDS given to staged K/V tiles */
   int32_t kv_tiles;             /* t_KV x d tiles resident in that share */
   int32_t stage_tiles;          /* t_KV x d tiles staged through registers per step */
+  int32_t score_tiles;          /* fp32 t_Q x t_KV score tiles live at once (2 when pipelined) */
   int32_t waves_per_wg;
   int32_t waves_per_simd;       /* resident waves per SIMD; divides the register file */
   int32_t vgpr_fixed;           /* registers per lane outside the counted arrays */
@@ -155,6 +156,24 @@ int attn_fwd_plan(const attn_hw_desc_t* hw, int B, int H, int L, int d, int caus
  * overlap in time on different streams must not share it: serialise them). */
 int attn_fwd(const void* Q, const void* K, const void* V, void* O,
              int B, int H, int L, int d, float scale, int causal, int dtype, void* stream);
+
+/* The two halves of attn_fwd, for callers that own the workspace (and for
+ * timing the fused kernel on its own).  Split-N (Section 4.3): when the
+ * derivation splits the key range, attn_fwd_partial runs the fused kernel
+ * and leaves each split's unnormalised output, running max and running sum
+ * in `workspace` (fp32 [n_split][B*H][L][d] followed by [n_split][B*H][L][2]);
+ * attn_fwd_merge folds them with the associative merge and writes O.
+ * Without a split the required workspace is 0 bytes, attn_fwd_partial writes
+ * O itself and attn_fwd_merge does nothing.  attn_fwd_workspace_bytes gives
+ * the size for the current device; the workspace must be 16-byte aligned
+ * (ATTN_E_WORKSPACE / ATTN_E_ALIGN otherwise).  attn_fwd_partial followed
+ * by attn_fwd_merge on one stream equals attn_fwd bit for bit. */
+int attn_fwd_workspace_bytes(int B, int H, int L, int d, int causal, int dtype, size_t* out);
+int attn_fwd_partial(const void* Q, const void* K, const void* V, void* O,
+                     int B, int H, int L, int d, float scale, int causal, int dtype,
+                     void* workspace, size_t workspace_bytes, void* stream);
+int attn_fwd_merge(const void* workspace, size_t workspace_bytes, void* O,
+                   int B, int H, int L, int d, float scale, int causal, int dtype, void* stream);
 
 /* Unfused baseline (Section 5.4, Table 3): three kernels on `stream` --
  * S = scale Q K^T written to the workspace in `dtype`, a row softmax

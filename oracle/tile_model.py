@@ -10,9 +10,9 @@ the paper's CU-centric order (Section 4):
    (Table 2: t_KV = 64 at d=128, 128 at d=64 with fp32 elements).
 2. VGPR -> Q tile per wave.  Every array live at the synchronisation point
    between the two GEMMs is counted (Section 5.2, Table 2 caption): the Q
-   operand, the fp32 score tile, the fp32 output accumulator and the running
-   (m, delta) pair, plus the registers used to stage the next K/V tile and a
-   fixed overhead.  t_Q is the largest multiple of the atom width whose count
+   operand, the fp32 score tile(s), the fp32 output accumulator and the
+   running (m, delta) pair, plus the registers used to stage the next K/V tile
+   and a fixed overhead.  t_Q is the largest multiple of the atom width whose count
    fits the per-wave budget (Section 4, "VGPR constraint").  The count
    reproduces all four rows of Table 2 with the paper's fp32 instance.
 3. CU count -> grid.  If fewer workgroups than CUs result, the derivation
@@ -67,6 +67,7 @@ class Structure:
     kv_lds_den: int = 1      # ... as the fraction num/den
     kv_tiles: int = 1        # t_KV x d tiles resident in that share
     stage_tiles: int = 0     # t_KV x d tiles passed through VGPRs per step
+    score_tiles: int = 1     # fp32 score tiles live at once (2 when the loop is pipelined)
     waves_per_wg: int = 1
     waves_per_simd: int = 1  # resident waves per SIMD (divides the register file)
     vgpr_fixed: int = 16     # addresses, loop state, operand staging
@@ -81,7 +82,7 @@ def vgpr_count(hw, atom, op, st, t_q, t_kv, n_w):
     """Registers per lane live at the GEMM1/GEMM2 synchronisation point."""
     wf = hw.wavefront_size
     q_reg = _cdiv(t_q * op.d * op.elem_bytes, 4 * wf)        # Q operand
-    s_reg = _cdiv(t_q * t_kv * atom.acc_bytes, 4 * wf)       # score tile, fp32
+    s_reg = st.score_tiles * _cdiv(t_q * t_kv * atom.acc_bytes, 4 * wf)  # score tiles, fp32
     o_reg = _cdiv(t_q * op.d * atom.acc_bytes, 4 * wf)       # output accumulator, fp32
     stats = 2 * _cdiv(t_q, atom.n)                           # running max and sum
     stage = _cdiv(st.stage_tiles * t_kv * op.d * op.elem_bytes, 4 * wf * n_w)

@@ -29,7 +29,8 @@ CODE = {v: k for k, v in STATUS.items()}
 # Every function the header declares; the CPU tests check each is exported.
 EXPORTS = (
     "attn_hw_desc_preset", "attn_hw_desc_query", "attn_atom_preset", "attn_fwd_op",
-    "attn_vgpr_estimate", "attn_tile_derive", "attn_fwd_plan", "attn_fwd", "attn_fwd_unfused",
+    "attn_vgpr_estimate", "attn_tile_derive", "attn_fwd_plan", "attn_fwd", "attn_fwd_workspace_bytes",
+    "attn_fwd_partial", "attn_fwd_merge", "attn_fwd_unfused",
     "attn_unfused_workspace_bytes", "attn_mfma_probe", "attn_strerror",
 )
 
@@ -62,7 +63,7 @@ class Atom(_Struct):
 class Op(_Struct):
     _fields_ = [("B", c_int32), ("H", c_int32), ("L", c_int32), ("d", c_int32),
                 ("elem_bytes", c_int32), ("causal", c_int32), ("kv_lds_num", c_int32),
-                ("kv_lds_den", c_int32), ("kv_tiles", c_int32), ("stage_tiles", c_int32),
+                ("kv_lds_den", c_int32), ("kv_tiles", c_int32), ("stage_tiles", c_int32), ("score_tiles", c_int32),
                 ("waves_per_wg", c_int32), ("waves_per_simd", c_int32), ("vgpr_fixed", c_int32),
                 ("max_split", c_int32)]
 
@@ -103,6 +104,11 @@ def load():
         "attn_fwd_plan": (c_int, [P(HwDesc), c_int, c_int, c_int, c_int, c_int, c_int, P(TileReport)]),
         "attn_fwd": (c_int, [c_void_p, c_void_p, c_void_p, c_void_p, c_int, c_int, c_int, c_int,
                              c_float, c_int, c_int, c_void_p]),
+        "attn_fwd_workspace_bytes": (c_int, [c_int, c_int, c_int, c_int, c_int, c_int, P(c_size_t)]),
+        "attn_fwd_partial": (c_int, [c_void_p, c_void_p, c_void_p, c_void_p, c_int, c_int, c_int, c_int,
+                                     c_float, c_int, c_int, c_void_p, c_size_t, c_void_p]),
+        "attn_fwd_merge": (c_int, [c_void_p, c_size_t, c_void_p, c_int, c_int, c_int, c_int, c_float, c_int,
+                                   c_int, c_void_p]),
         "attn_fwd_unfused": (c_int, [c_void_p, c_void_p, c_void_p, c_void_p, c_int, c_int, c_int,
                                      c_int, c_float, c_int, c_int, c_void_p, c_size_t, c_void_p]),
         "attn_unfused_workspace_bytes": (c_size_t, [c_int, c_int, c_int, c_int]),
@@ -214,6 +220,32 @@ def attn_fwd(q, k, v, o, scale: float, causal: bool, stream=None):
             raise AttnError(CODE["ATTN_E_SHAPE"], "q, k, v, o must share shape and dtype")
     _check(load().attn_fwd(_dev_ptr(q), _dev_ptr(k), _dev_ptr(v), _dev_ptr(o), B, H, L, d,
                            float(scale), int(causal), dtype_code(q), _stream_ptr(q, stream)))
+
+
+def attn_fwd_workspace_bytes(B, H, L, d, causal, dtype) -> int:
+    out = c_size_t()
+    _check(load().attn_fwd_workspace_bytes(B, H, L, d, int(causal), dtype, ctypes.byref(out)))
+    return out.value
+
+
+def _ws(workspace):
+    if workspace is None:
+        return None, 0
+    return _dev_ptr(workspace), workspace.numel() * workspace.element_size()
+
+
+def attn_fwd_partial(q, k, v, o, scale: float, causal: bool, workspace=None, stream=None):
+    B, H, L, d = q.shape
+    ws, nb = _ws(workspace)
+    _check(load().attn_fwd_partial(_dev_ptr(q), _dev_ptr(k), _dev_ptr(v), _dev_ptr(o), B, H, L, d, float(scale),
+                                   int(causal), dtype_code(q), ws, nb, _stream_ptr(q, stream)))
+
+
+def attn_fwd_merge(workspace, o, scale: float, causal: bool, stream=None):
+    B, H, L, d = o.shape
+    ws, nb = _ws(workspace)
+    _check(load().attn_fwd_merge(ws, nb, _dev_ptr(o), B, H, L, d, float(scale), int(causal), dtype_code(o),
+                                 _stream_ptr(o, stream)))
 
 
 def attn_fwd_unfused(q, k, v, o, scale: float, causal: bool, workspace, stream=None):

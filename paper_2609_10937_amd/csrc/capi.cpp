@@ -23,13 +23,13 @@ namespace {
 
 // Fixed structure of the fused kernel family in fwd_kernel.hpp: all of LDS
 // holds a ring of 5 stages of (K tile, V tile) filled by direct HBM->LDS
-// copies (no registers stage them), 8 waves per workgroup at 2 waves per
-// SIMD.  vgpr_fixed covers what the count does not name (operand fragments
-// in flight, addresses, loop state, mask bookkeeping): the smallest value for
-// which every tile the derivation accepts compiles without spilling (the
-// d=64, 48-rows-per-wave kernel needs more than 256 registers, which a
-// fixed term of 83 or more excludes).
-constexpr int kKvLdsNum = 1, kKvLdsDen = 1, kKvTiles = 10, kStageTiles = 0;
+// copies (no registers stage them), one fp32 score tile live at a time, 8
+// waves per workgroup at 2 waves per SIMD.  vgpr_fixed covers what the count
+// does not name (operand fragments in flight, addresses, loop state): the
+// smallest value for which every tile the derivation accepts compiles
+// without spilling (the d=64, 48-rows-per-wave kernel needs more than 256
+// registers, which a fixed term of 83 or more excludes).
+constexpr int kKvLdsNum = 1, kKvLdsDen = 1, kKvTiles = 10, kStageTiles = 0, kScoreTiles = 1;
 constexpr int kWavesPerWg = 8, kWavesPerSimd = 2, kVgprFixed = 83, kMaxSplit = 16;
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
@@ -84,7 +84,7 @@ attn_mfma_atom_t atom_for(int dtype) {
 struct DeviceState {
   bool have_desc = false;
   attn_hw_desc_t desc{};
-  void* ws = nullptr;
+  void* ws = nullptr;  // split partial results for attn_fwd
   size_t ws_bytes = 0;
 };
 
@@ -142,6 +142,7 @@ int make_op(int B, int H, int L, int d, int causal, int dtype, attn_op_t* op) {
   op->kv_lds_den = kKvLdsDen;
   op->kv_tiles = kKvTiles;
   op->stage_tiles = kStageTiles;
+  op->score_tiles = kScoreTiles;
   op->waves_per_wg = kWavesPerWg;
   op->waves_per_simd = kWavesPerSimd;
   op->vgpr_fixed = kVgprFixed;
@@ -163,6 +164,55 @@ int plan(const attn_hw_desc_t* hw, int B, int H, int L, int d, int causal, int d
   if (inst) *inst = f;
   if (rep->grid > 0x7fffffffLL) return ATTN_E_SHAPE;
   return ATTN_OK;
+}
+
+// Checks, derivation and kernel parameters shared by the forward entry
+// points (no device memory is touched).
+struct Prepared {
+  attn_tile_report_t rep;
+  const FwdInstance* inst;
+  FwdParams p;
+  size_t ws_bytes;  // split workspace the plan needs (0 without a split)
+};
+
+int prepare(const void* Q, const void* K, const void* V, void* O, int B, int H, int L, int d, float scale, int causal,
+            int dtype, Prepared* out) {
+  int rc = check_tensors(Q, K, V, O);
+  if (rc != ATTN_OK) return rc;
+  rc = check_shape(B, H, L, d, dtype);
+  if (rc != ATTN_OK) return rc;
+  rc = check_scale(scale);
+  if (rc != ATTN_OK) return rc;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return ATTN_E_HIP;
+  attn_hw_desc_t desc;
+  rc = device_desc(dev, &desc);
+  if (rc != ATTN_OK) return rc;
+  rc = plan(&desc, B, H, L, d, causal, dtype, &out->rep, &out->inst);
+  if (rc != ATTN_OK) return rc;
+  FwdParams& p = out->p;
+  p = FwdParams{};
+  p.q = Q;
+  p.k = K;
+  p.v = V;
+  p.o = O;
+  p.BH = B * H;
+  p.L = L;
+  p.n_qt = (L + out->rep.tile_q - 1) / out->rep.tile_q;
+  p.n_split = out->rep.n_split;
+  const int n_kv = (L + out->rep.t_kv - 1) / out->rep.t_kv;
+  p.tiles_per_split = (n_kv + out->rep.n_split - 1) / out->rep.n_split;
+  p.causal = causal != 0;
+  p.c = scale * 1.4426950408889634f;
+  const size_t rows = (size_t)p.n_split * p.BH * L;
+  out->ws_bytes = p.n_split > 1 ? rows * (size_t)d * 4 + rows * 8 : 0;
+  return ATTN_OK;
+}
+
+void bind_workspace(FwdParams& p, void* ws, int d) {
+  const size_t rows = (size_t)p.n_split * p.BH * p.L;
+  p.part_o = static_cast<float*>(ws);
+  p.part_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + rows * (size_t)d * 4);
 }
 
 }  // namespace
@@ -266,44 +316,16 @@ int attn_fwd_plan(const attn_hw_desc_t* hw, int B, int H, int L, int d, int caus
 
 int attn_fwd(const void* Q, const void* K, const void* V, void* O, int B, int H, int L, int d, float scale,
              int causal, int dtype, void* stream) {
-  int rc = check_tensors(Q, K, V, O);
+  Prepared pr;
+  int rc = prepare(Q, K, V, O, B, H, L, d, scale, causal, dtype, &pr);
   if (rc != ATTN_OK) return rc;
-  rc = check_shape(B, H, L, d, dtype);
-  if (rc != ATTN_OK) return rc;
-  rc = check_scale(scale);
-  if (rc != ATTN_OK) return rc;
-
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return ATTN_E_HIP;
-  attn_hw_desc_t desc;
-  rc = device_desc(dev, &desc);
-  if (rc != ATTN_OK) return rc;
-  attn_tile_report_t rep;
-  const FwdInstance* inst = nullptr;
-  rc = plan(&desc, B, H, L, d, causal, dtype, &rep, &inst);
-  if (rc != ATTN_OK) return rc;
-
-  FwdParams p{};
-  p.q = Q;
-  p.k = K;
-  p.v = V;
-  p.o = O;
-  p.BH = B * H;
-  p.L = L;
-  p.n_qt = (L + rep.tile_q - 1) / rep.tile_q;
-  p.n_split = rep.n_split;
-  const int n_kv = (L + rep.t_kv - 1) / rep.t_kv;
-  p.tiles_per_split = (n_kv + rep.n_split - 1) / rep.n_split;
-  p.causal = causal != 0;
-  p.c = scale * 1.4426950408889634f;
   hipStream_t s = static_cast<hipStream_t>(stream);
-
-  if (p.n_split > 1) {
-    const size_t rows = (size_t)p.n_split * p.BH * L;
-    const size_t need = rows * (size_t)d * 4 + rows * 8;
+  if (pr.ws_bytes > 0) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return ATTN_E_HIP;
     std::lock_guard<std::mutex> lk(g_mu);
     DeviceState& st = g_dev[dev];
-    if (st.ws_bytes < need) {
+    if (st.ws_bytes < pr.ws_bytes) {
       // Every earlier use of the old buffer was enqueued on some stream; wait
       // for the device before releasing it.
       if (st.ws) {
@@ -312,16 +334,52 @@ int attn_fwd(const void* Q, const void* K, const void* V, void* O, int B, int H,
         st.ws = nullptr;
         st.ws_bytes = 0;
       }
-      if (hipMalloc(&st.ws, need) != hipSuccess) return ATTN_E_HIP;
-      st.ws_bytes = need;
+      if (hipMalloc(&st.ws, pr.ws_bytes) != hipSuccess) return ATTN_E_HIP;
+      st.ws_bytes = pr.ws_bytes;
     }
-    p.part_o = static_cast<float*>(st.ws);
-    p.part_ml = reinterpret_cast<float*>(static_cast<char*>(st.ws) + rows * (size_t)d * 4);
+    bind_workspace(pr.p, st.ws, d);
   }
-
-  if (inst->launch(p, (unsigned)rep.grid, s) != hipSuccess) return ATTN_E_HIP;
-  if (p.n_split > 1 && launch_combine(p, d, dtype, s) != hipSuccess) return ATTN_E_HIP;
+  if (pr.inst->launch(pr.p, (unsigned)pr.rep.grid, s) != hipSuccess) return ATTN_E_HIP;
+  if (pr.p.n_split > 1 && launch_combine(pr.p, d, dtype, s) != hipSuccess) return ATTN_E_HIP;
   return ATTN_OK;
+}
+
+int attn_fwd_workspace_bytes(int B, int H, int L, int d, int causal, int dtype, size_t* out) {
+  if (!out) return ATTN_E_NULLPTR;
+  *out = 0;
+  const void* fake = reinterpret_cast<const void*>((uintptr_t)1 << 20);  // passes the pointer checks
+  Prepared pr;
+  const int rc = prepare(fake, fake, fake, const_cast<void*>(fake), B, H, L, d, 1.0f, causal, dtype, &pr);
+  if (rc != ATTN_OK) return rc;
+  *out = pr.ws_bytes;
+  return ATTN_OK;
+}
+
+int attn_fwd_partial(const void* Q, const void* K, const void* V, void* O, int B, int H, int L, int d, float scale,
+                     int causal, int dtype, void* workspace, size_t workspace_bytes, void* stream) {
+  Prepared pr;
+  int rc = prepare(Q, K, V, O, B, H, L, d, scale, causal, dtype, &pr);
+  if (rc != ATTN_OK) return rc;
+  if (pr.ws_bytes > 0) {
+    if (!workspace || workspace_bytes < pr.ws_bytes) return ATTN_E_WORKSPACE;
+    if (!aligned16(workspace)) return ATTN_E_ALIGN;
+    bind_workspace(pr.p, workspace, d);
+  }
+  return pr.inst->launch(pr.p, (unsigned)pr.rep.grid, static_cast<hipStream_t>(stream)) == hipSuccess ? ATTN_OK
+                                                                                                   : ATTN_E_HIP;
+}
+
+int attn_fwd_merge(const void* workspace, size_t workspace_bytes, void* O, int B, int H, int L, int d, float scale,
+                   int causal, int dtype, void* stream) {
+  const void* fake = reinterpret_cast<const void*>((uintptr_t)1 << 20);
+  Prepared pr;
+  int rc = prepare(fake, fake, fake, O, B, H, L, d, scale, causal, dtype, &pr);
+  if (rc != ATTN_OK) return rc;
+  if (pr.ws_bytes == 0) return ATTN_OK;  // the partial call already wrote O
+  if (!workspace || workspace_bytes < pr.ws_bytes) return ATTN_E_WORKSPACE;
+  if (!aligned16(workspace)) return ATTN_E_ALIGN;
+  bind_workspace(pr.p, const_cast<void*>(workspace), d);
+  return launch_combine(pr.p, d, dtype, static_cast<hipStream_t>(stream)) == hipSuccess ? ATTN_OK : ATTN_E_HIP;
 }
 
 size_t attn_unfused_workspace_bytes(int B, int H, int L, int dtype) {

@@ -135,10 +135,24 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-// 16-byte chunk swizzles of a row-major [rows][KCH chunks] tile.
+// 16-byte chunk swizzles of a row-major [rows][KCH chunks] tile (KCH = 16
+// for d = 128, 8 for d = 64), chosen so that every operand read of the
+// kernel hits distinct LDS banks:
+//  K (GEMM1 A operand, ds_read_b128): 16 lanes read 16 consecutive rows at
+//    one logical chunk -> distinct physical chunks across rows.
+//  V (GEMM2 A operand, ds_read_b64_tr_b16): a 32-lane pair of groups reads
+//    rows base + 0..3 and base + 4..7, two adjacent chunks each -> the row's
+//    low three bits select distinct chunk positions.
 template <int KCH>
-__device__ __forceinline__ int k_swz(int r) { return r & (KCH - 1); }
-__device__ __forceinline__ int v_swz(int r) { return 2 * (r & 3); }
+__device__ __forceinline__ int k_swz(int r) {
+  if constexpr (KCH == 16) return r & 15;
+  else return (r >> 1) & 7;
+}
+template <int KCH>
+__device__ __forceinline__ int v_swz(int r) {
+  if constexpr (KCH == 16) return (2 * (r & 3)) | (8 * ((r >> 2) & 1));
+  else return 2 * ((r >> 1) & 3);
+}
 
 // Online-softmax step of Algorithm 1 for one tile of scores s (S^T
 // fragments, raw logits): row maxima, the lazily raised reference max, the
@@ -282,7 +296,7 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
       const size_t row = (size_t)min(kv0 + r, L - 1) * D;
       __builtin_amdgcn_global_load_lds((ATTN_GLOBAL void*)(Kh + row + ((pc ^ k_swz<KCH>(r)) * 8)),
                                        (ATTN_LDS void*)(ks + blk * 512), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds((ATTN_GLOBAL void*)(Vh + row + ((pc ^ v_swz(r)) * 8)),
+      __builtin_amdgcn_global_load_lds((ATTN_GLOBAL void*)(Vh + row + ((pc ^ v_swz<KCH>(r)) * 8)),
                                        (ATTN_LDS void*)(vs + blk * 512), 16, 0, 0);
     }
   };
@@ -375,7 +389,7 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
 #pragma unroll
           for (int h = 0; h < 2; ++h) {
             const int R = 32 * pp + 16 * h + 4 * g + (c >> 2);
-            const int phys = (col >> 3) ^ v_swz(R);
+            const int phys = (col >> 3) ^ v_swz<KCH>(R);
             half[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
                 (ATTN_LDS i16x4_t*)(Vs + R * D + phys * 8 + cpart));
           }

@@ -6,7 +6,7 @@
 //      kernel structure gives them (Section 4, LDS constraint).
 //   2. The register budget fixes the query rows per wave, counting every array
 //      live at the synchronisation point between the two products: the Q
-//      operand, the fp32 score tile, the fp32 output accumulator and the
+//      operand, the fp32 score tile(s), the fp32 output accumulator and the
 //      running max/sum, plus staging registers and a fixed overhead
 //      (Section 5.4, Table 2 caption; Section 4, VGPR constraint).
 //   3. The CU count bounds the grid from below: split the key range (the
@@ -31,7 +31,7 @@ int64_t vgpr_estimate(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, co
                       int64_t t_q, int64_t t_kv, int64_t n_w) {
   const int64_t lane_words = 4 * (int64_t)hw->wavefront_size;  // bytes in one register across a wave
   const int64_t q_operand = cdiv(t_q * op->d * op->elem_bytes, lane_words);
-  const int64_t scores = cdiv(t_q * t_kv * atom->acc_bytes, lane_words);
+  const int64_t scores = op->score_tiles * cdiv(t_q * t_kv * atom->acc_bytes, lane_words);
   const int64_t out_acc = cdiv(t_q * op->d * atom->acc_bytes, lane_words);
   const int64_t stats = 2 * cdiv(t_q, atom->n);
   const int64_t staging = cdiv((int64_t)op->stage_tiles * t_kv * op->d * op->elem_bytes, lane_words * n_w);
@@ -52,7 +52,7 @@ int derive_tiles(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const a
   if (atom->m <= 0 || atom->n <= 0 || atom->k <= 0 || atom->in_bytes <= 0 || atom->acc_bytes <= 0)
     return ATTN_E_ARG;
   if (op->B <= 0 || op->H <= 0 || op->L <= 0 || op->d <= 0 || op->elem_bytes <= 0) return ATTN_E_ARG;
-  if (op->kv_lds_num <= 0 || op->kv_lds_den <= 0 || op->kv_tiles <= 0 || op->stage_tiles < 0 ||
+  if (op->kv_lds_num <= 0 || op->kv_lds_den <= 0 || op->kv_tiles <= 0 || op->stage_tiles < 0 || op->score_tiles < 1 ||
       op->waves_per_wg <= 0 || op->waves_per_simd <= 0 || op->vgpr_fixed < 0 || op->max_split < 1)
     return ATTN_E_ARG;
 
@@ -89,7 +89,7 @@ int derive_tiles(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const a
   //    slope = (d*elem + t_kv*acc + d*acc) / (4*wf) + 2/n.
   int64_t n_w = op->waves_per_wg;
   const double lw = 4.0 * hw->wavefront_size;
-  const double slope = ((double)op->d * op->elem_bytes + (double)t_kv * atom->acc_bytes +
+  const double slope = ((double)op->d * op->elem_bytes + (double)op->score_tiles * t_kv * atom->acc_bytes +
                         (double)op->d * atom->acc_bytes) / lw + 2.0 / atom->n;
   const double intercept = (double)op->stage_tiles * t_kv * op->d * op->elem_bytes / (lw * n_w) +
                            op->vgpr_fixed;

@@ -54,7 +54,7 @@ def _to_c(hw, atom, op, st):
     a = capi.Atom(m=atom.m, n=atom.n, k=atom.k, in_bytes=atom.in_bytes, acc_bytes=atom.acc_bytes)
     o = capi.Op(B=op.B, H=op.H, L=op.L, d=op.d, elem_bytes=op.elem_bytes, causal=int(op.causal),
                 kv_lds_num=st.kv_lds_num, kv_lds_den=st.kv_lds_den, kv_tiles=st.kv_tiles,
-                stage_tiles=st.stage_tiles, waves_per_wg=st.waves_per_wg,
+                stage_tiles=st.stage_tiles, score_tiles=st.score_tiles, waves_per_wg=st.waves_per_wg,
                 waves_per_simd=st.waves_per_simd, vgpr_fixed=st.vgpr_fixed, max_split=st.max_split)
     return h, a, o
 
@@ -80,7 +80,7 @@ def test_table2_through_the_library():
     atom = capi.attn_atom_preset("f32_16x16x4")
     for r in g["table2"]:
         op = capi.Op(B=1, H=1, L=16384, d=r["d"], elem_bytes=4, causal=0, kv_lds_num=1, kv_lds_den=2,
-                     kv_tiles=1, stage_tiles=0, waves_per_wg=1, waves_per_simd=1, vgpr_fixed=16,
+                     kv_tiles=1, stage_tiles=0, score_tiles=1, waves_per_wg=1, waves_per_simd=1, vgpr_fixed=16,
                      max_split=1)
         rc, rep = capi.attn_tile_derive(hw, atom, op)
         assert rc == 0 and rep.t_kv == r["t_kv"]
@@ -108,6 +108,7 @@ op_s = stg.builds(T.Op, B=stg.integers(1, 8), H=stg.integers(1, 64),
                   elem_bytes=stg.sampled_from([2, 4]), causal=stg.booleans())
 st_s = stg.builds(T.Structure, kv_lds_num=stg.just(1), kv_lds_den=stg.sampled_from([1, 2, 4]),
                   kv_tiles=stg.sampled_from([1, 2, 4, 8]), stage_tiles=stg.sampled_from([0, 1, 2]),
+                  score_tiles=stg.sampled_from([1, 2]),
                   waves_per_wg=stg.sampled_from([1, 2, 4, 8, 16]),
                   waves_per_simd=stg.sampled_from([1, 2, 4]),
                   vgpr_fixed=stg.integers(0, 128), max_split=stg.sampled_from([1, 2, 8, 16]))
@@ -184,6 +185,20 @@ def test_unfused_rejects_bad_arguments(lib):
     assert f(P, P, P, P, 1, 1, 12, 64, 0.1, 0, 0, P, ws, None) == capi.CODE["ATTN_E_SHAPE"]
     assert f(None, P, P, P, 1, 1, 16, 64, 0.1, 0, 0, P, ws, None) == capi.CODE["ATTN_E_NULLPTR"]
     assert capi.attn_unfused_workspace_bytes(0, 1, 16, 0) == 0
+
+
+def test_partial_and_merge_reject_bad_arguments(lib):
+    f = lib.attn_fwd_partial
+    assert f(None, P, P, P, 1, 1, 16, 64, 0.1, 0, 0, None, 0, None) == capi.CODE["ATTN_E_NULLPTR"]
+    assert f(P, P, P, P, 1, 1, 16, 96, 0.1, 0, 0, None, 0, None) == capi.CODE["ATTN_E_UNSUPPORTED_D"]
+    assert f(P, P, P, P, 1, 1, 16, 64, -0.1, 0, 0, None, 0, None) == capi.CODE["ATTN_E_SCALE"]
+    g = lib.attn_fwd_merge
+    assert g(None, 0, None, 1, 1, 16, 64, 0.1, 0, 0, None) == capi.CODE["ATTN_E_NULLPTR"]
+    assert g(None, 0, P, 0, 1, 16, 64, 0.1, 0, 0, None) == capi.CODE["ATTN_E_SHAPE"]
+    out = ctypes.c_size_t(7)
+    assert lib.attn_fwd_workspace_bytes(1, 1, 16, 80, 0, 0, ctypes.byref(out)) == capi.CODE["ATTN_E_UNSUPPORTED_D"]
+    assert out.value == 0
+    assert lib.attn_fwd_workspace_bytes(1, 1, 16, 64, 0, 0, None) == capi.CODE["ATTN_E_NULLPTR"]
 
 
 def test_probe_rejects_bad_arguments(lib):

@@ -159,6 +159,30 @@ def test_gpu_invariants():
         _gpu.assert_close(oc, prefix, "bf16", "uniform causal weights")
 
 
+@pytest.mark.parametrize("name", ["single_head_l16384_d128", "h8_l1024_d128", "tiny_f16_l128_d64"])
+def test_partial_then_merge_equals_fused(name):
+    """attn_fwd_partial + attn_fwd_merge with a caller workspace == attn_fwd, bit for bit."""
+    w = inputs.WORKLOADS[name]
+    print(f"case partial+merge {name}", flush=True)
+    q, k, v = (_gpu.upload(x, w.dtype) for x in inputs.workload_inputs(w))
+    a = _gpu.fused(q, k, v, w.scale, w.causal)
+    dt = capi.ATTN_BF16 if w.dtype == "bf16" else capi.ATTN_F16
+    nb = capi.attn_fwd_workspace_bytes(w.B, w.H, w.L, w.d, w.causal, dt)
+    plan = capi.attn_fwd_plan(w.B, w.H, w.L, w.d, w.causal, dt)
+    assert (nb > 0) == (plan.n_split > 1)
+    ws = torch.empty(max(nb, 16), dtype=torch.uint8, device="cuda") if nb else None
+    b = torch.empty_like(q)
+    capi.attn_fwd_partial(q, k, v, b, w.scale, w.causal, ws)
+    capi.attn_fwd_merge(ws, b, w.scale, w.causal)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    if nb:
+        small = torch.empty(nb - 16, dtype=torch.uint8, device="cuda")
+        with pytest.raises(capi.AttnError) as e:
+            capi.attn_fwd_partial(q, k, v, b, w.scale, w.causal, small)
+        assert e.value.status == capi.CODE["ATTN_E_WORKSPACE"]
+
+
 def test_bitwise_deterministic():
     print("case determinism", flush=True)
     w = inputs.WORKLOADS["single_head_l16384_d128"]
