@@ -30,21 +30,30 @@
 // reads of a 16-lane group touch distinct banks.  Tiles move HBM -> LDS with
 // global_load_lds_dwordx4 (lane l of a wave writes bytes 16l..16l+15 of a
 // 1 KB block; each lane picks the source chunk that belongs at its slot), so
-// no registers stage them and nothing is transposed on the way.  Up to
-// ST-2 tiles beyond the one being computed are in flight; one barrier per
-// tile.
+// no registers stage them and nothing is transposed on the way.
+//
+// Schedule.  A step of a wave is a matrix phase (GEMM2 of the previous tile
+// and GEMM1 of the current one: 64 products plus 4 for the row sums) and a
+// vector phase (the softmax of the current tile).  With two waves per SIMD
+// the two run one phase apart (ping-pong): while one issues matrix products
+// the other issues the exponentials, which is the overlap a single wave
+// cannot get because its own vector work waits for its products.  Every
+// phase ends with a workgroup barrier; the operand reads of a matrix phase
+// are software-pipelined PF fragments ahead of the products that use them.
 //
 // Softmax bookkeeping keeps a per-row reference max m that is only raised
-// when a new row maximum exceeds it by more than 2^TAU in the exponent (the
-// merge of Section 4.3 holds for any common reference point, so the result is
-// the same; exponentiated weights stay below 2^TAU).  Most tiles then need no
-// rescaling of O.  The row sum adds the 16-bit weights that enter the second
-// product (v_dot2 with ones), so the weights the output is normalised by are
-// exactly the ones applied to V.
+// when a score would give a weight above 2^8 (the merge of Section 4.3 holds
+// for any common reference point, so the result is the same).  Most tiles
+// then need neither row maxima nor rescaling of O.  The row sums come from
+// the second product itself (a block of ones times the packed weights), so
+// the weights the output is normalised by are exactly the 16-bit weights
+// applied to V.
 #pragma once
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <type_traits>
 
 #include "internal.h"
 
@@ -62,6 +71,8 @@ typedef short i16x8_t __attribute__((ext_vector_type(8)));
 
 #define ATTN_LDS __attribute__((address_space(3)))
 #define ATTN_GLOBAL __attribute__((address_space(1)))
+// Lambdas of the kernel body: always inlined (a call would spill live state).
+#define ATTN_INLINE __attribute__((always_inline))
 
 template <int DT>
 struct Mfma;
@@ -74,11 +85,6 @@ struct Mfma<ATTN_BF16> {
   static __device__ __forceinline__ f32x4_t run(V8 a, V8 b, f32x4_t c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
   }
-  // a.x + a.y (+ acc), exact products with one, fp32 accumulation
-  static __device__ __forceinline__ float sum2(V2 a, float acc) {
-    const V2 one = {(__bf16)1.0f, (__bf16)1.0f};
-    return __builtin_amdgcn_fdot2_f32_bf16(a, one, acc, false);
-  }
 };
 
 template <>
@@ -89,11 +95,11 @@ struct Mfma<ATTN_F16> {
   static __device__ __forceinline__ f32x4_t run(V8 a, V8 b, f32x4_t c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
   }
-  static __device__ __forceinline__ float sum2(V2 a, float acc) {
-    const V2 one = {(_Float16)1.0f, (_Float16)1.0f};
-    return __builtin_amdgcn_fdot2(a, one, acc, false);
-  }
 };
+
+// Two 16-bit ones packed in a 32-bit word.
+template <int DT>
+constexpr uint32_t kOne2 = DT == ATTN_BF16 ? 0x3F803F80u : 0x3C003C00u;
 
 __device__ __forceinline__ u32x4_t ldg16(const uint16_t* p) {
   return *reinterpret_cast<const u32x4_t*>(p);
@@ -112,15 +118,6 @@ __device__ __forceinline__ float max_across_rows(float x) {
   return fmaxf(__builtin_bit_cast(float, (uint32_t)b[0]), __builtin_bit_cast(float, (uint32_t)b[1]));
 }
 
-__device__ __forceinline__ float sum_across_rows(float x) {
-  const uint32_t u = __builtin_bit_cast(uint32_t, x);
-  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
-  const float y = __builtin_bit_cast(float, (uint32_t)a[0]) + __builtin_bit_cast(float, (uint32_t)a[1]);
-  const uint32_t v = __builtin_bit_cast(uint32_t, y);
-  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
-  return __builtin_bit_cast(float, (uint32_t)b[0]) + __builtin_bit_cast(float, (uint32_t)b[1]);
-}
-
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
 // vmcnt[3:0] in bits 3:0, vmcnt[5:4] in bits 15:14; expcnt and lgkmcnt at max).
 template <int N>
@@ -129,10 +126,33 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
+// One 16-byte-per-lane copy from global memory straight into LDS
+// (global_load_lds_dwordx4): lane l's 16 bytes at base + off land at LDS byte
+// address lds_dst + 16 l.  The LDS address goes through M0, which needs one
+// wait state before the copy reads it.  Written as inline assembly so that the compiler
+// does not treat every later LDS read as depending on the copy: completion
+// is tracked here with explicit vector-memory counter waits and barriers.
+__device__ __forceinline__ void copy_to_lds(const void* base, uint32_t off, uint32_t lds_dst) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "s"(lds_dst)
+               : "memory", "m0");
+}
+// The same copy for the tile that crosses the end of the sequence (per-lane
+// clamped offsets).  A distinct instruction string keeps the compiler from
+// merging the two paths into one with selects on every copy.
+__device__ __forceinline__ void copy_to_lds_edge(const void* base, uint32_t off, uint32_t lds_dst) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1 ; edge tile" ::"v"(off), "s"(base),
+               "s"(lds_dst)
+               : "memory", "m0");
+}
+
 // Workgroup barrier that orders LDS accesses but leaves in-flight
 // global->LDS copies alone (the compiler's __syncthreads would drain them).
 __device__ __forceinline__ void lds_barrier() {
+  // Scheduling fences on both sides: no instruction may be moved across a
+  // phase boundary (the asm statement alone only orders memory operations).
+  __builtin_amdgcn_sched_barrier(0);
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
 }
 
 // 16-byte chunk swizzles of a row-major [rows][KCH chunks] tile (KCH = 16
@@ -155,13 +175,20 @@ __device__ __forceinline__ int v_swz(int r) {
 }
 
 // Online-softmax step of Algorithm 1 for one tile of scores s (S^T
-// fragments, raw logits): row maxima, the lazily raised reference max, the
-// 16-bit weights packed as the B operand of the second product, and the row
-// sums of those weights.  MASK = true for tiles crossing the causal diagonal
-// or the end of the sequence.
-template <bool MASK, typename M, int NKB, int NP, int QB, int NDB>
+// fragments, raw logits): the 16-bit weights exp(scale (s - m)) packed as the
+// B operand of the second product.  The reference m of a row can be any
+// common point for all of its keys (the merge of Section 4.3 holds for every
+// choice), so it only moves when a weight would exceed 2^8: each lane checks
+// its own scores against m + 8 / (scale log2 e) and only if one passes (or a
+// row has no reference yet) are the row maxima taken and the reference
+// raised to them; the accumulated output and row sums are then rescaled by
+// corr in the next matrix phase.  The row sums themselves are formed by the
+// second product (a block of ones times the packed weights), so they add
+// exactly the 16-bit weights that multiply V.  MASK = true for tiles
+// crossing the causal diagonal or the end of the sequence.
+template <bool MASK, typename M, int NKB, int NP, int QB>
 __device__ __forceinline__ void softmax_tile(f32x4_t (&s)[NKB][QB], typename M::V8 (&pk)[NP][QB], float (&m)[QB],
-                                             float (&l)[QB], f32x4_t (&o)[QB][NDB], int kv0, int q0, int g, int c,
+                                             float (&corr)[QB], bool& rescale, int kv0, int q0, int g, int c,
                                              int L, int causal, float cs, float thr) {
   using V2 = typename M::V2;
   using S = typename M::S;
@@ -179,27 +206,27 @@ __device__ __forceinline__ void softmax_tile(f32x4_t (&s)[NKB][QB], typename M::
           if (!keep[kb][r]) s[kb][qb][r] = -INFINITY;
         }
     }
-    float mx = -INFINITY;
+    float mx = s[0][qb][0];
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb)
-      mx = fmaxf(fmaxf(mx, s[kb][qb][0]), fmaxf(fmaxf(s[kb][qb][1], s[kb][qb][2]), s[kb][qb][3]));
-    mx = max_across_rows(mx);
-    // Raise the reference only when an exponent would exceed TAU (and on a
-    // row's first visible key, whatever the scale).
+#pragma unroll
+      for (int r = (kb == 0 ? 1 : 0); r < 4; r += 2)
+        mx = (r + 1 < 4) ? fmaxf(mx, fmaxf(s[kb][qb][r], s[kb][qb][r + 1])) : fmaxf(mx, s[kb][qb][r]);
+    corr[qb] = 1.f;
     const float lim = (m[qb] == -INFINITY) ? -INFINITY : m[qb] + thr;
     if (__any(mx > lim)) {
+      mx = max_across_rows(mx);
       const float m_new = fmaxf(m[qb], mx);
-      const float corr = (m[qb] == -INFINITY) ? 0.f : exp2_hw((m[qb] - m_new) * cs);
-      l[qb] *= corr;
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) o[qb][db] *= corr;
-      m[qb] = m_new;
+      if (__any(m_new > m[qb])) {
+        corr[qb] = (m[qb] == -INFINITY) ? 0.f : exp2_hw((m[qb] - m_new) * cs);
+        m[qb] = m_new;
+        rescale = true;
+      }
     }
     const float mc = (m[qb] == -INFINITY) ? 0.f : m[qb] * cs;
-    float rs = l[qb];
 #pragma unroll
     for (int pp = 0; pp < NP; ++pp) {
-      V2 h2[4];
+      uint32_t wd[4];
 #pragma unroll
       for (int h = 0; h < 2; ++h)
 #pragma unroll
@@ -210,15 +237,10 @@ __device__ __forceinline__ void softmax_tile(f32x4_t (&s)[NKB][QB], typename M::
             e0 = keep[2 * pp + h][r] ? e0 : 0.f;
             e1 = keep[2 * pp + h][r + 1] ? e1 : 0.f;
           }
-          h2[2 * h + r / 2] = (V2){(S)e0, (S)e1};
+          wd[2 * h + r / 2] = __builtin_bit_cast(uint32_t, (V2){(S)e0, (S)e1});
         }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) rs = M::sum2(h2[j], rs);
-      pk[pp][qb] = __builtin_shufflevector(__builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3),
-                                           __builtin_shufflevector(h2[2], h2[3], 0, 1, 2, 3),
-                                           0, 1, 2, 3, 4, 5, 6, 7);
+      pk[pp][qb] = __builtin_bit_cast(typename M::V8, (u32x4_t){wd[0], wd[1], wd[2], wd[3]});
     }
-    l[qb] = rs;
   }
 }
 
@@ -226,7 +248,6 @@ template <int DT, int D, int TKV, int QB, int NW, int ST>
 __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   using M = Mfma<DT>;
   using V8 = typename M::V8;
-  using V2 = typename M::V2;
   using S = typename M::S;
   constexpr int TQW = 16 * QB;              // query rows per wave
   constexpr int TILE_Q = NW * TQW;          // query rows per workgroup
@@ -237,23 +258,33 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   constexpr int KCH = D / 8;                // 16-byte chunks per row
   constexpr int TILE = TKV * D;             // elements of one K or V tile
   constexpr int CHUNKS = TKV * KCH;
-  constexpr int LPW = CHUNKS / (NW * 64);   // 1 KB copies per wave per tile and tensor
-  constexpr float TAU = 8.0f;
+  constexpr int NCW = NW;                   // waves that copy tiles (all)
+  constexpr int LPW = CHUNKS / (NCW * 64);  // 1 KB copies per copying wave per tile and tensor
   static_assert(TKV % 32 == 0 && D % 32 == 0 && KCH >= 8 && (KCH & (KCH - 1)) == 0, "tile alignment");
-  static_assert(CHUNKS % (NW * 64) == 0, "tile copies must split evenly across waves");
-  // Tiles kept in flight beyond the one being computed: bounded by the ring
-  // (ST - 2) and by the 6-bit vector-memory counter (2*LPW copies per tile).
-  constexpr int DEPTH = (ST - 2) < 63 / (2 * LPW) ? (ST - 2) : 63 / (2 * LPW);
-  static_assert(ST >= 2 && DEPTH >= 0, "stages");
+  static_assert(CHUNKS % (NCW * 64) == 0, "tile copies must split evenly across waves");
+  // Tiles requested ahead.  In S(j) a wave requests its part of
+  // tile j + 1 + AHEAD, whose stage held tile j + 1 + AHEAD - ST; that V tile
+  // must have been read by both groups, i.e. in M(j - 1) at the latest,
+  // which allows ST - 3.  The 6-bit vector-memory counter (at most AHEAD
+  // tiles of 2 LPW copies outstanding) allows 63 / (2 LPW).
+  constexpr int AHEAD = (ST - 3) < 63 / (2 * LPW) ? (ST - 3) : 63 / (2 * LPW);
+  static_assert(ST >= 3 && AHEAD >= 1, "stages");
+  constexpr int NVF = NP * NDB;             // V^T fragments per tile (GEMM2 A operands)
+  constexpr int NKF = KC * NKB;             // K fragments per tile (GEMM1 A operands)
+  constexpr int PF = 6;                     // operand fragments loaded ahead of their use
 
   __shared__ __attribute__((aligned(1024))) uint16_t smem[ST * 2 * TILE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int w = tid >> 6;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4;
   const int c = lane & 15;
   const int L = p.L;
+  // Waves w and w + 4 of a workgroup share a SIMD.  With two waves per SIMD
+  // the second runs one workgroup phase behind the first, so that one issues
+  // matrix products while the other runs the softmax.
+  const int grp = NW == 8 ? (w >> 2) : 0;
 
   // Workgroup -> (query tile, head, split).  Heads vary fastest among
   // workgroups of one query-tile rank; causal launches heavy tiles first.
@@ -278,27 +309,76 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
     n_kv = min(n_kv, (last + TKV - 1) / TKV);
   }
   const int t_begin = split * p.tiles_per_split;
-  const int t_end = min(n_kv, t_begin + p.tiles_per_split);
+  const int n = min(n_kv, t_begin + p.tiles_per_split) - t_begin;  // tiles of this workgroup
 
-  // Copy tile t of K and V into stage `stage`: the wave's LPW 1 KB blocks of
-  // each tile image.  Image slot P holds row P/KCH, logical chunk
-  // (P%KCH) ^ swizzle(row).  Rows past the end are clamped to row L-1
-  // (finite data that the mask removes).
-  auto issue = [&](int t, int stage) {
-    const int kv0 = t * TKV;
-    uint16_t* ks = smem + stage * 2 * TILE;
-    uint16_t* vs = ks + TILE;
+  // LDS image: stage st holds the K tile at byte st*STAGEB and the V tile
+  // TILEB after it, each row-major [TKV][D] in 16-byte chunks, chunk
+  // positions XOR-swizzled per row (k_swz / v_swz).
+  constexpr int ROWB = D * 2;               // bytes per K/V row
+  constexpr int TILEB = TKV * ROWB;         // bytes per K or V tile
+  constexpr int STAGEB = 2 * TILEB;
+  ATTN_LDS char* const lds = (ATTN_LDS char*)smem;
+  const uint32_t lds0 = (uint32_t)(size_t)lds;
+
+  // Copy tile j (relative to t_begin) of K and V into stage j % ST: the
+  // copying wave's LPW 1 KB blocks of each tile image.  Image slot P holds
+  // row P/KCH, logical chunk (P%KCH) ^ swizzle(row).  The byte offsets of a
+  // lane's sources within a tile are fixed, so each copy is a wave-uniform
+  // tile base plus a 32-bit lane offset.  In the tile that crosses the end
+  // of the sequence, rows past the end are clamped to row L-1 (finite data
+  // that the mask removes).
+  // Block b of a tile image (1 KB) holds rows b*RPB .. b*RPB + RPB - 1.  A
+  // copying wave cw takes blocks cw, cw + NCW, cw + 2 NCW, ...; when NCW * RPB is
+  // a multiple of 16 rows (the period of both swizzles) its lanes' source
+  // offsets differ between those blocks by a constant, so one offset per
+  // tensor serves all of them.
+  constexpr int RPB = 1024 / ROWB;
+  constexpr bool SHIFT = (NCW * RPB) % 16 == 0;
+  const int cw = w;  // index among the copying waves
+  uint32_t koff[SHIFT ? 1 : LPW], voff[SHIFT ? 1 : LPW];
 #pragma unroll
-    for (int i = 0; i < LPW; ++i) {
-      const int blk = w * LPW + i;
-      const int P = blk * 64 + lane;
-      const int r = P / KCH, pc = P % KCH;
-      const size_t row = (size_t)min(kv0 + r, L - 1) * D;
-      __builtin_amdgcn_global_load_lds((ATTN_GLOBAL void*)(Kh + row + ((pc ^ k_swz<KCH>(r)) * 8)),
-                                       (ATTN_LDS void*)(ks + blk * 512), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds((ATTN_GLOBAL void*)(Vh + row + ((pc ^ v_swz<KCH>(r)) * 8)),
-                                       (ATTN_LDS void*)(vs + blk * 512), 16, 0, 0);
+  for (int i = 0; i < (SHIFT ? 1 : LPW); ++i) {
+    const int P = (i * NCW + cw) * 64 + lane;
+    const int r = P / KCH, pc = P % KCH;
+    koff[i] = (uint32_t)(r * ROWB + ((pc ^ k_swz<KCH>(r)) * 16));
+    voff[i] = (uint32_t)(r * ROWB + ((pc ^ v_swz<KCH>(r)) * 16));
+  }
+  auto ko = [&](int i) ATTN_INLINE { return SHIFT ? koff[0] + (uint32_t)(i * NCW * 1024) : koff[SHIFT ? 0 : i]; };
+  auto vo = [&](int i) ATTN_INLINE { return SHIFT ? voff[0] + (uint32_t)(i * NCW * 1024) : voff[SHIFT ? 0 : i]; };
+  // This wave's part of tile j: its LPW blocks of the K image and of the V
+  // image.  With SHIFT the per-block source offsets differ by a constant,
+  // added to the wave-uniform base instead of the lane offset.
+  auto issue = [&](int j) ATTN_INLINE {
+    const int kv0 = (t_begin + j) * TKV;
+    const uint32_t kdst = (uint32_t)__builtin_amdgcn_readfirstlane(lds0 + (j % ST) * STAGEB) + cw * 1024;
+    const char* ksrc = reinterpret_cast<const char*>(Kh) + (size_t)kv0 * ROWB;
+    const char* vsrc = reinterpret_cast<const char*>(Vh) + (size_t)kv0 * ROWB;
+    if (kv0 + TKV <= L) {
+#pragma unroll
+      for (int i = 0; i < LPW; ++i) {
+        const int step = SHIFT ? i * NCW * 1024 : 0;
+        copy_to_lds(ksrc + step, SHIFT ? koff[0] : koff[SHIFT ? 0 : i], kdst + i * NCW * 1024);
+        copy_to_lds(vsrc + step, SHIFT ? voff[0] : voff[SHIFT ? 0 : i], kdst + TILEB + i * NCW * 1024);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < LPW; ++i) {
+        const int r = ((i * NCW + cw) * 64 + lane) / KCH;
+        const uint32_t back = (uint32_t)(max(0, kv0 + r - (L - 1)) * ROWB);  // bytes back to row L-1
+        copy_to_lds_edge(ksrc, ko(i) - back, kdst + i * NCW * 1024);
+        copy_to_lds_edge(vsrc, vo(i) - back, kdst + TILEB + i * NCW * 1024);
+      }
     }
+  };
+  // This wave's copies of tile j are complete once no more than the copies
+  // of the tiles requested after it are outstanding (vector-memory
+  // operations retire in issue order).
+  auto wait_tile = [&](int j, int last_issued) ATTN_INLINE {
+    const int after = last_issued - j;
+    if (after >= 3) wait_vmcnt<(AHEAD >= 3 ? 6 * LPW : 0)>();
+    else if (after == 2) wait_vmcnt<(AHEAD >= 2 ? 4 * LPW : 0)>();
+    else if (after == 1) wait_vmcnt<2 * LPW>();
+    else wait_vmcnt<0>();
   };
 
   // Q fragments: B operand of S^T = K Q^T, one 16-byte load per (block, k step).
@@ -315,100 +395,193 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   }
   // Drain the Q loads here: the loop's waits count only tile copies.
   wait_vmcnt<0>();
-#pragma unroll
-  for (int j = 0; j <= DEPTH; ++j)
-    if (t_begin + j < t_end) issue(t_begin + j, j);
 
   f32x4_t o[QB][NDB];
-  float m[QB], l[QB];
+  f32x4_t lacc[QB];  // row sums of the weights (all four entries of a lane equal)
+  float m[QB];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     m[qb] = -INFINITY;
-    l[qb] = 0.f;
+    lacc[qb] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int db = 0; db < NDB; ++db) o[qb][db] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
   }
+  // A raised reference max rescales the accumulated output by corr; the
+  // softmax only records it, and the next matrix phase applies it before
+  // adding the tile's products (so the vector phase never rewrites o).
+  float corr[QB];
+  bool rescale = false;
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) corr[qb] = 1.f;
+  f32x4_t s[NKB][QB];  // scores of the tile between its GEMM1 and its softmax
+  V8 pk[NP][QB];       // 16-bit weights of the tile between its softmax and its GEMM2
 
   const float cs = p.c;
-  const float thr = TAU / cs;  // +inf when cs == 0: the reference never moves
-  int stage = 0;
-  for (int t = t_begin; t < t_end; ++t) {
-    // This wave's copies of tile t are complete once no more than the copies
-    // of the tiles issued after it (up to DEPTH tiles) are outstanding;
-    // vector-memory operations retire in issue order.
-    const int after = min(DEPTH, t_end - 1 - t);
-    if (after >= DEPTH) wait_vmcnt<2 * LPW * DEPTH>();
-    else if (after == 2) wait_vmcnt<(DEPTH > 2 ? 4 * LPW : 0)>();
-    else if (after == 1) wait_vmcnt<(DEPTH > 1 ? 2 * LPW : 0)>();
-    else wait_vmcnt<0>();
-    lds_barrier();  // tile t visible to all waves; every wave is done with tile t-1
-    if (t + DEPTH + 1 < t_end) {
-      const int st_next = stage + DEPTH + 1 >= ST ? stage + DEPTH + 1 - ST : stage + DEPTH + 1;
-      issue(t + DEPTH + 1, st_next);
-    }
+  const float thr = 8.0f / cs;  // weights stay <= 2^8; +inf when cs == 0 (every weight is 1)
 
-    const int kv0 = t * TKV;
-    // Wave-uniform: skip waves with no valid row or whose rows all precede the tile.
-    const bool live = (q0 < L) && !(p.causal && kv0 > q0 + TQW - 1);
-    if (live) {
-      const uint16_t* Ks = smem + stage * 2 * TILE;
-      const uint16_t* Vs = Ks + TILE;
-      const bool need_mask = (kv0 + TKV > L) || (p.causal && kv0 + TKV - 1 > q0);
+  // Operand fragments.  V^T (GEMM2 A operand, 16 d x 32 keys): lane c
+  // addresses row 4g + c/4 (+16 for the upper half) and column
+  // 16db + 4(c%4) of the row-major V tile; the transposing read hands it
+  // four keys of one column.  K (GEMM1 A operand, 16 keys x 32 d): one
+  // 16-byte read of row 16kb + c.  Neither swizzle depends on the row bits
+  // that pp, h or kb set, and db (kc) enters a lane's byte address only
+  // through the bits 32*db (64*kc), XORed with the lane's swizzle: so the
+  // address is a lane base XOR a per-fragment constant, plus a row offset
+  // that the read instruction carries.
+  static_assert(ROWB >= 256 || KC * 64 <= ROWB, "operand address bits");
+  uint32_t kbase, vbase;
+  {
+    kbase = (uint32_t)(c * ROWB + ((g ^ k_swz<KCH>(c)) & 3) * 16 + ((k_swz<KCH>(c) >> 2) * 64));
+    const int R0 = 4 * g + (c >> 2);
+    const int sw = v_swz<KCH>(R0);
+    vbase = (uint32_t)(R0 * ROWB + (((c & 3) >> 1) ^ (sw & 1)) * 16 + (sw >> 1) * 32 + 8 * (c & 1));
+  }
+  auto load_v = [&](uint32_t vb, int pp, int db) ATTN_INLINE -> V8 {
+    ATTN_LDS const char* base = (ATTN_LDS const char*)(size_t)(vb ^ (uint32_t)(32 * db));
+    const i16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4_t*)(base + (32 * pp) * ROWB));
+    const i16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4_t*)(base + (32 * pp + 16) * ROWB));
+    const i16x8_t cat = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return __builtin_bit_cast(V8, cat);
+  };
+  auto load_k = [&](uint32_t kb0, int kc, int kb) ATTN_INLINE -> V8 {
+    ATTN_LDS const char* base = (ATTN_LDS const char*)(size_t)(kb0 ^ (uint32_t)(64 * kc));
+    return __builtin_bit_cast(V8, *(ATTN_LDS const u32x4_t*)(base + kb * 16 * ROWB));
+  };
 
-      // GEMM1: s[kb][qb][r] = <K[kv0 + 16kb + 4g + r], Q[q0 + 16qb + c]>
-      f32x4_t s[NKB][QB];
+  // The stage offsets pass through readfirstlane: as opaque wave-uniform
+  // values they stay one scalar add per phase instead of becoming one
+  // induction variable per fragment address.
+  auto mphase = [&](auto g2c, auto g1c, int j) ATTN_INLINE {
+    constexpr bool G2 = decltype(g2c)::value, G1 = decltype(g1c)::value;
+    constexpr int F = (G2 ? NVF : 0) + (G1 ? NKF : 0);
+    const uint32_t Vs = vbase + (uint32_t)__builtin_amdgcn_readfirstlane(lds0 + ((j + ST - 1) % ST) * STAGEB + TILEB);
+    const uint32_t Ks = kbase + (uint32_t)__builtin_amdgcn_readfirstlane(lds0 + (j % ST) * STAGEB);
+    auto load = [&](int f) ATTN_INLINE -> V8 {
+      if (G2 && f < NVF) return load_v(Vs, f / NDB, f % NDB);
+      const int fk = f - (G2 ? NVF : 0);
+      return load_k(Ks, fk / NKB, fk % NKB);
+    };
+    if (G2 && rescale) {
 #pragma unroll
-      for (int kb = 0; kb < NKB; ++kb) {
+      for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb) s[kb][qb] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
-        const int row = 16 * kb + c;
-#pragma unroll
-        for (int kc = 0; kc < KC; ++kc) {
-          const int phys = (4 * kc + g) ^ k_swz<KCH>(row);
-          const V8 kf = __builtin_bit_cast(V8, *reinterpret_cast<const u32x4_t*>(Ks + row * D + phys * 8));
-#pragma unroll
-          for (int qb = 0; qb < QB; ++qb) s[kb][qb] = M::run(kf, qf[qb][kc], s[kb][qb]);
-        }
+        for (int db = 0; db < NDB; ++db) o[qb][db] *= corr[qb];
+        lacc[qb] *= corr[qb];
       }
-
-      V8 pk[NP][QB];
-      if (need_mask)
-        softmax_tile<true, M>(s, pk, m, l, o, kv0, q0, g, c, L, p.causal, cs, thr);
-      else
-        softmax_tile<false, M>(s, pk, m, l, o, kv0, q0, g, c, L, p.causal, cs, thr);
-
-      // GEMM2: o[qb][db][r] += sum_k V^T[16db + 4g + r][k] P^T[k][q]
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        // lane c addresses row 4g + c/4 (+16 for the upper half), column 16db + 4(c%4)
-        const int col = 16 * db + 4 * (c & 3);
-        const int cpart = 4 * (c & 1);
-#pragma unroll
-        for (int pp = 0; pp < NP; ++pp) {
-          i16x4_t half[2];
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const int R = 32 * pp + 16 * h + 4 * g + (c >> 2);
-            const int phys = (col >> 3) ^ v_swz<KCH>(R);
-            half[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                (ATTN_LDS i16x4_t*)(Vs + R * D + phys * 8 + cpart));
-          }
-          const i16x8_t cat = {half[0][0], half[0][1], half[0][2], half[0][3],
-                               half[1][0], half[1][1], half[1][2], half[1][3]};
-          const V8 va = __builtin_bit_cast(V8, cat);
-#pragma unroll
-          for (int qb = 0; qb < QB; ++qb) o[qb][db] = M::run(va, pk[pp][qb], o[qb][db]);
-        }
-      }
+      rescale = false;
     }
-    stage = (stage + 1 == ST) ? 0 : stage + 1;
+    V8 buf[F];
+#pragma unroll
+    for (int f = 0; f < PF && f < F; ++f) buf[f] = load(f);
+    // Row sums of the previous tile's weights: a 16 x 32 block of ones times
+    // P^T, while the first operand reads are in flight.
+    if constexpr (G2) {
+      const V8 ones = __builtin_bit_cast(V8, (u32x4_t){kOne2<DT>, kOne2<DT>, kOne2<DT>, kOne2<DT>});
+#pragma unroll
+      for (int pp = 0; pp < NP; ++pp)
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) lacc[qb] = M::run(ones, pk[pp][qb], lacc[qb]);
+    }
+#pragma unroll
+    for (int f = 0; f < F; ++f) {
+      if (G2 && f < NVF) {
+        const int pp = f / NDB, db = f % NDB;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) o[qb][db] = M::run(buf[f], pk[pp][qb], o[qb][db]);
+      } else {
+        const int fk = f - (G2 ? NVF : 0);
+        const int kc = fk / NKB, kb = fk % NKB;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+          s[kb][qb] = M::run(buf[f], qf[qb][kc], kc == 0 ? (f32x4_t){0.f, 0.f, 0.f, 0.f} : s[kb][qb]);
+      }
+      if (f + PF < F) buf[f + PF] = load(f + PF);
+    }
+    // Keep that order through instruction scheduling: the first PF
+    // fragments' reads, then per fragment its QB products and the reads of
+    // the fragment PF places later (a V^T fragment is two reads).
+    auto reads_of = [](int f) ATTN_INLINE {
+      if (G2 && f < NVF) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // DS reads
+      else __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    };
+#pragma unroll
+    for (int f = 0; f < PF && f < F; ++f) reads_of(f);
+    if constexpr (G2) __builtin_amdgcn_sched_group_barrier(0x008, NP * QB, 0);  // row-sum products
+#pragma unroll
+    for (int f = 0; f < F; ++f) {
+      __builtin_amdgcn_sched_group_barrier(0x008, QB, 0);  // matrix products
+      if (f + PF < F) reads_of(f + PF);
+    }
+  };
+
+  // Vector phase S(j): the softmax of tile j.  Only tiles that cross the
+  // causal diagonal or the end of the sequence take the masked body.
+  auto sphase = [&](int j) ATTN_INLINE {
+    const int kv0 = (t_begin + j) * TKV;
+    if ((kv0 + TKV > L) || (p.causal && kv0 + TKV - 1 > q0))
+      softmax_tile<true, M>(s, pk, m, corr, rescale, kv0, q0, g, c, L, p.causal, cs, thr);
+    else
+      softmax_tile<false, M>(s, pk, m, corr, rescale, kv0, q0, g, c, L, p.causal, cs, thr);
+  };
+
+  // Phase schedule.  Step j of a wave is its matrix phase M(j) = GEMM2 of
+  // tile j-1 and GEMM1 of tile j, then its vector phase S(j); each phase
+  // ends with a workgroup barrier.  Group 1 starts one phase later than
+  // group 0 (an idle first phase) and group 0 ends with an idle phase, so
+  // both pass 2n + 4 barriers and the two waves of a SIMD are always in
+  // different kinds of phase.  Every wave computes every tile of the range:
+  // a wave whose rows all precede a tile (causal) sees only masked keys
+  // there and adds nothing, which keeps one straight path through the loop.
+  //
+  // Every wave requests its part of tile j + 1 + AHEAD at the start of S(j)
+  // and waits for its copies of tile j + 2 at the end of it.  The requested
+  // tile's stage held tile j + 1 + AHEAD - ST <= j - 2, whose V tile was
+  // last read in M(j - 1), which both groups have finished when either
+  // starts S(j); tile j + 2 is first read in M(j + 2), after the barriers
+  // that end S(j) of both groups.
+  if (n > 0) {
+    // Tiles 0 and 1 are needed first; the next ones follow once they have
+    // landed, so that no more than AHEAD tiles' copies are ever outstanding.
+    issue(0);
+    if constexpr (4 * LPW > 63) wait_vmcnt<0>();
+    if (1 < n) issue(1);
+    wait_vmcnt<0>();
+    for (int j = 2; j <= AHEAD && j < n; ++j) issue(j);
+    lds_barrier();
+    if (grp == 1) lds_barrier();
+    auto vector_phase = [&](int j) ATTN_INLINE {
+      if (j + 1 + AHEAD < n) issue(j + 1 + AHEAD);
+      sphase(j);
+      if (j + 2 < n) wait_tile(j + 2, min(n - 1, j + 1 + AHEAD));
+      lds_barrier();
+    };
+    // Step 0: GEMM1 of the first tile only.
+    __builtin_amdgcn_s_setprio(1);
+    mphase(std::false_type{}, std::true_type{}, 0);
+    __builtin_amdgcn_s_setprio(0);
+    lds_barrier();
+    vector_phase(0);
+    for (int j = 1; j < n; ++j) {
+      __builtin_amdgcn_s_setprio(1);
+      mphase(std::true_type{}, std::true_type{}, j);
+      __builtin_amdgcn_s_setprio(0);
+      lds_barrier();
+      vector_phase(j);
+    }
+    // Step n: GEMM2 of the last tile, then an idle vector phase.
+    __builtin_amdgcn_s_setprio(1);
+    mphase(std::true_type{}, std::false_type{}, n);
+    __builtin_amdgcn_s_setprio(0);
+    lds_barrier();
+    lds_barrier();
+    if (grp == 0) lds_barrier();
   }
 
   // Epilogue.  Each of the four lane groups holds a partial row sum over its
   // key subset (same reference max), so the total is their sum.
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
-    const float lt = sum_across_rows(l[qb]);
+    const float lt = lacc[qb][0];
     const int q = q0 + 16 * qb + c;
     if (p.n_split == 1) {
       const float inv = lt > 0.f ? 1.f / lt : 0.f;
