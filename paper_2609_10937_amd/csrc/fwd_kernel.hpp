@@ -132,16 +132,24 @@ __device__ __forceinline__ void wait_vmcnt() {
 // wait state before the copy reads it.  Written as inline assembly so that the compiler
 // does not treat every later LDS read as depending on the copy: completion
 // is tracked here with explicit vector-memory counter waits and barriers.
+// base and lds_dst are wave-uniform; they pass through readfirstlane so that
+// they are scalar operands whatever the compiler can prove.
+__device__ __forceinline__ uint64_t uniform_ptr(const void* p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  return ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(v >> 32)) << 32) |
+         (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)v);
+}
 __device__ __forceinline__ void copy_to_lds(const void* base, uint32_t off, uint32_t lds_dst) {
-  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "s"(lds_dst)
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(uniform_ptr(base)),
+               "s"(__builtin_amdgcn_readfirstlane(lds_dst))
                : "memory", "m0");
 }
 // The same copy for the tile that crosses the end of the sequence (per-lane
 // clamped offsets).  A distinct instruction string keeps the compiler from
 // merging the two paths into one with selects on every copy.
 __device__ __forceinline__ void copy_to_lds_edge(const void* base, uint32_t off, uint32_t lds_dst) {
-  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1 ; edge tile" ::"v"(off), "s"(base),
-               "s"(lds_dst)
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1 ; edge tile" ::"v"(off),
+               "s"(uniform_ptr(base)), "s"(__builtin_amdgcn_readfirstlane(lds_dst))
                : "memory", "m0");
 }
 
