@@ -160,8 +160,10 @@ int attn_fwd(const void* Q, const void* K, const void* V, void* O,
 /* The two halves of attn_fwd, for callers that own the workspace (and for
  * timing the fused kernel on its own).  Split-N (Section 4.3): when the
  * derivation splits the key range, attn_fwd_partial runs the fused kernel
- * and leaves each split's unnormalised output, running max and running sum
- * in `workspace` (fp32 [n_split][B*H][L][d] followed by [n_split][B*H][L][2]);
+ * and leaves each split's unnormalised output, reference point and running
+ * sum in `workspace` (fp32 [n_split][B*H][L][d] followed by
+ * [n_split][B*H][L][2]; the reference is scale*log2(e) times a logit at or
+ * below the row's maximum, -inf for a row that saw no key);
  * attn_fwd_merge folds them with the associative merge and writes O.
  * Without a split the required workspace is 0 bytes, attn_fwd_partial writes
  * O itself and attn_fwd_merge does nothing.  attn_fwd_workspace_bytes gives

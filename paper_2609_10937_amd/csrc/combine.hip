@@ -1,5 +1,7 @@
 // Merge of key-range partial results (Section 4.3, the associative operator
 // on (max, sum) extended to the output accumulator, applied across splits).
+// Each split's reference point is stored in the base-2 domain (scale log2 e
+// times a logit), so the weights are plain powers of two.
 // One thread per (row, 4 consecutive output columns).
 #include "fwd_kernel.hpp"
 
@@ -23,7 +25,7 @@ __global__ void __launch_bounds__(256) combine_kernel(const FwdParams p) {
   for (int s = 0; s < p.n_split; ++s) {
     const float ms = p.part_ml[(s * stride + row) * 2];
     const float ls = p.part_ml[(s * stride + row) * 2 + 1];
-    const float wgt = (ms == -INFINITY) ? 0.f : exp2_hw((ms - m) * p.c);
+    const float wgt = (ms == -INFINITY) ? 0.f : exp2_hw(ms - m);
     lt += wgt * ls;
     const f32x4_t po = *reinterpret_cast<const f32x4_t*>(p.part_o + (s * stride + row) * D + 4 * d4);
     acc += wgt * po;

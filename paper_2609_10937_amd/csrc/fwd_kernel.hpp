@@ -182,36 +182,46 @@ __device__ __forceinline__ int v_swz(int r) {
   else return 2 * ((r >> 1) & 3);
 }
 
-// Online-softmax step of Algorithm 1 for one tile of scores s (S^T
-// fragments, raw logits): the 16-bit weights exp(scale (s - m)) packed as the
-// B operand of the second product.  The reference m of a row can be any
-// common point for all of its keys (the merge of Section 4.3 holds for every
-// choice), so it only moves when a weight would exceed 2^8: each lane checks
-// its own scores against m + 8 / (scale log2 e) and only if one passes (or a
-// row has no reference yet) are the row maxima taken and the reference
-// raised to them; the accumulated output and row sums are then rescaled by
-// corr in the next matrix phase.  The row sums themselves are formed by the
-// second product (a block of ones times the packed weights), so they add
-// exactly the 16-bit weights that multiply V.  MASK = true for tiles
-// crossing the causal diagonal or the end of the sequence.
-template <bool MASK, typename M, int NKB, int NP, int QB>
-__device__ __forceinline__ void softmax_tile(f32x4_t (&s)[NKB][QB], typename M::V8 (&pk)[NP][QB], float (&m)[QB],
-                                             float (&corr)[QB], bool& rescale, int kv0, int q0, int g, int c,
-                                             int L, int causal, float cs, float thr) {
+// Online-softmax step of Algorithm 1 for one tile.  On entry s holds the raw
+// scores of the tile (S^T fragments); one fma each brings them to the base-2
+// domain relative to the row's reference point mref (cs = scale log2 e; the
+// product is not pre-scaled through Q, whose rounding to 16 bits would
+// double the error of the scores).  The reference of
+// a row can be any common point for all of its keys (the merge of Section 4.3
+// holds for every choice), so it only moves when a weight would exceed 2^8:
+// each lane checks its own scores against lim (8, or -inf while the row has
+// no reference yet) and only if one passes are the row maxima taken and the
+// reference raised to them; the tile's scores are shifted by the same amount
+// and the accumulated output and row sums are rescaled by corr in the next
+// matrix phase.  Out: the 16-bit weights 2^s packed as the B operand of the
+// second product.  The row sums are formed by the second product itself (a
+// block of ones times the packed weights), so they add exactly the 16-bit
+// weights that multiply V.  MASK = true for tiles crossing the causal
+// diagonal or the end of the sequence.  hook(qb) runs before row block qb
+// (the vector phase spreads its tile copies over the softmax with it).
+template <bool MASK, typename M, int NKB, int NP, int QB, typename Hook>
+__device__ __forceinline__ void softmax_tile(f32x4_t (&s)[NKB][QB], typename M::V8 (&pk)[NP][QB], float (&mref)[QB],
+                                             float (&lim)[QB], float (&corr)[QB], bool& rescale, int kv0, int q0,
+                                             int g, int c, int L, int causal, float cs, Hook&& hook) {
   using V2 = typename M::V2;
   using S = typename M::S;
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
+    __builtin_amdgcn_sched_barrier(0);
+    hook(qb);
+    __builtin_amdgcn_sched_barrier(0);
     const int q = q0 + 16 * qb + c;
-    bool keep[NKB][4];
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) s[kb][qb][r] = __builtin_fmaf(s[kb][qb][r], cs, -mref[qb]);
     if constexpr (MASK) {
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int kv = kv0 + 16 * kb + 4 * g + r;
-          keep[kb][r] = kv < L && !(causal && kv > q);
-          if (!keep[kb][r]) s[kb][qb][r] = -INFINITY;
+          if (!(kv < L && !(causal && kv > q))) s[kb][qb][r] = -INFINITY;
         }
     }
     float mx = s[0][qb][0];
@@ -220,18 +230,21 @@ __device__ __forceinline__ void softmax_tile(f32x4_t (&s)[NKB][QB], typename M::
 #pragma unroll
       for (int r = (kb == 0 ? 1 : 0); r < 4; r += 2)
         mx = (r + 1 < 4) ? fmaxf(mx, fmaxf(s[kb][qb][r], s[kb][qb][r + 1])) : fmaxf(mx, s[kb][qb][r]);
-    corr[qb] = 1.f;
-    const float lim = (m[qb] == -INFINITY) ? -INFINITY : m[qb] + thr;
-    if (__any(mx > lim)) {
+    if (__any(mx > lim[qb])) {
       mx = max_across_rows(mx);
-      const float m_new = fmaxf(m[qb], mx);
-      if (__any(m_new > m[qb])) {
-        corr[qb] = (m[qb] == -INFINITY) ? 0.f : exp2_hw((m[qb] - m_new) * cs);
-        m[qb] = m_new;
+      const bool has = lim[qb] != -INFINITY;
+      // New reference: the row maximum if above the old one; a row without
+      // a reference takes its maximum as is (nothing has been accumulated).
+      const float delta = has ? fmaxf(mx, 0.f) : (mx == -INFINITY ? 0.f : mx);
+      if (__any(delta != 0.f)) {
+        corr[qb] = has ? exp2_hw(-delta) : 0.f;
+        mref[qb] += delta;
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) s[kb][qb] -= delta;
         rescale = true;
       }
+      if (mx != -INFINITY) lim[qb] = 8.f;
     }
-    const float mc = (m[qb] == -INFINITY) ? 0.f : m[qb] * cs;
 #pragma unroll
     for (int pp = 0; pp < NP; ++pp) {
       uint32_t wd[4];
@@ -239,12 +252,8 @@ __device__ __forceinline__ void softmax_tile(f32x4_t (&s)[NKB][QB], typename M::
       for (int h = 0; h < 2; ++h)
 #pragma unroll
         for (int r = 0; r < 4; r += 2) {
-          float e0 = exp2_hw(__builtin_fmaf(s[2 * pp + h][qb][r], cs, -mc));
-          float e1 = exp2_hw(__builtin_fmaf(s[2 * pp + h][qb][r + 1], cs, -mc));
-          if constexpr (MASK) {
-            e0 = keep[2 * pp + h][r] ? e0 : 0.f;
-            e1 = keep[2 * pp + h][r + 1] ? e1 : 0.f;
-          }
+          const float e0 = exp2_hw(s[2 * pp + h][qb][r]);
+          const float e1 = exp2_hw(s[2 * pp + h][qb][r + 1]);
           wd[2 * h + r / 2] = __builtin_bit_cast(uint32_t, (V2){(S)e0, (S)e1});
         }
       pk[pp][qb] = __builtin_bit_cast(typename M::V8, (u32x4_t){wd[0], wd[1], wd[2], wd[3]});
@@ -354,27 +363,32 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   auto ko = [&](int i) ATTN_INLINE { return SHIFT ? koff[0] + (uint32_t)(i * NCW * 1024) : koff[SHIFT ? 0 : i]; };
   auto vo = [&](int i) ATTN_INLINE { return SHIFT ? voff[0] + (uint32_t)(i * NCW * 1024) : voff[SHIFT ? 0 : i]; };
   // This wave's part of tile j: its LPW blocks of the K image and of the V
-  // image.  With SHIFT the per-block source offsets differ by a constant,
-  // added to the wave-uniform base instead of the lane offset.
-  auto issue = [&](int j) ATTN_INLINE {
+  // image, as copies 0 .. NC-1 (copy 2i is block i of K, 2i+1 block i of V);
+  // issue(j, lo, hi) makes copies lo .. hi-1.  With SHIFT the per-block
+  // source offsets differ by a constant, added to the wave-uniform base
+  // instead of the lane offset.
+  constexpr int NC = 2 * LPW;
+  auto issue = [&](int j, int lo, int hi) ATTN_INLINE {
     const int kv0 = (t_begin + j) * TKV;
     const uint32_t kdst = (uint32_t)__builtin_amdgcn_readfirstlane(lds0 + (j % ST) * STAGEB) + cw * 1024;
     const char* ksrc = reinterpret_cast<const char*>(Kh) + (size_t)kv0 * ROWB;
     const char* vsrc = reinterpret_cast<const char*>(Vh) + (size_t)kv0 * ROWB;
     if (kv0 + TKV <= L) {
 #pragma unroll
-      for (int i = 0; i < LPW; ++i) {
+      for (int ci = lo; ci < hi; ++ci) {
+        const int i = ci >> 1;
         const int step = SHIFT ? i * NCW * 1024 : 0;
-        copy_to_lds(ksrc + step, SHIFT ? koff[0] : koff[SHIFT ? 0 : i], kdst + i * NCW * 1024);
-        copy_to_lds(vsrc + step, SHIFT ? voff[0] : voff[SHIFT ? 0 : i], kdst + TILEB + i * NCW * 1024);
+        if (ci & 1) copy_to_lds(vsrc + step, SHIFT ? voff[0] : voff[SHIFT ? 0 : i], kdst + TILEB + i * NCW * 1024);
+        else copy_to_lds(ksrc + step, SHIFT ? koff[0] : koff[SHIFT ? 0 : i], kdst + i * NCW * 1024);
       }
     } else {
 #pragma unroll
-      for (int i = 0; i < LPW; ++i) {
+      for (int ci = lo; ci < hi; ++ci) {
+        const int i = ci >> 1;
         const int r = ((i * NCW + cw) * 64 + lane) / KCH;
         const uint32_t back = (uint32_t)(max(0, kv0 + r - (L - 1)) * ROWB);  // bytes back to row L-1
-        copy_to_lds_edge(ksrc, ko(i) - back, kdst + i * NCW * 1024);
-        copy_to_lds_edge(vsrc, vo(i) - back, kdst + TILEB + i * NCW * 1024);
+        if (ci & 1) copy_to_lds_edge(vsrc, vo(i) - back, kdst + TILEB + i * NCW * 1024);
+        else copy_to_lds_edge(ksrc, ko(i) - back, kdst + i * NCW * 1024);
       }
     }
   };
@@ -388,6 +402,8 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
     else if (after == 1) wait_vmcnt<2 * LPW>();
     else wait_vmcnt<0>();
   };
+
+  const float cs = p.c;  // scale * log2(e): scores in the base-2 domain
 
   // Q fragments: B operand of S^T = K Q^T, one 16-byte load per (block, k step).
   V8 qf[QB][KC];
@@ -406,26 +422,26 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
 
   f32x4_t o[QB][NDB];
   f32x4_t lacc[QB];  // row sums of the weights (all four entries of a lane equal)
-  float m[QB];
+  // Per row: the reference point in the base-2 domain (cs times a logit) and
+  // the check limit (-inf until the row has seen a key, then 8).
+  float mref[QB], lim[QB];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
-    m[qb] = -INFINITY;
+    mref[qb] = 0.f;
+    lim[qb] = -INFINITY;
     lacc[qb] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int db = 0; db < NDB; ++db) o[qb][db] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
   }
-  // A raised reference max rescales the accumulated output by corr; the
-  // softmax only records it, and the next matrix phase applies it before
-  // adding the tile's products (so the vector phase never rewrites o).
+  // A raised reference rescales the accumulated output by corr; the softmax
+  // only records it, and the next matrix phase applies it before adding the
+  // tile's products (so the vector phase never rewrites o) and resets corr.
   float corr[QB];
   bool rescale = false;
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) corr[qb] = 1.f;
   f32x4_t s[NKB][QB];  // scores of the tile between its GEMM1 and its softmax
   V8 pk[NP][QB];       // 16-bit weights of the tile between its softmax and its GEMM2
-
-  const float cs = p.c;
-  const float thr = 8.0f / cs;  // weights stay <= 2^8; +inf when cs == 0 (every weight is 1)
 
   // Operand fragments.  V^T (GEMM2 A operand, 16 d x 32 keys): lane c
   // addresses row 4g + c/4 (+16 for the upper half) and column
@@ -475,6 +491,7 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
 #pragma unroll
         for (int db = 0; db < NDB; ++db) o[qb][db] *= corr[qb];
         lacc[qb] *= corr[qb];
+        corr[qb] = 1.f;
       }
       rescale = false;
     }
@@ -524,12 +541,18 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
 
   // Vector phase S(j): the softmax of tile j.  Only tiles that cross the
   // causal diagonal or the end of the sequence take the masked body.
-  auto sphase = [&](int j) ATTN_INLINE {
+  // Its hook spreads this wave's copies of tile jc over the row blocks, so
+  // that the copies of the workgroup's waves do not all queue at once.
+  auto sphase = [&](int j, int jc) ATTN_INLINE {
     const int kv0 = (t_begin + j) * TKV;
+    auto hook = [&](int qb) ATTN_INLINE {
+      constexpr int per = NC % QB == 0 ? NC / QB : NC;
+      if (jc < n && qb * per < NC) issue(jc, qb * per, qb * per + per);
+    };
     if ((kv0 + TKV > L) || (p.causal && kv0 + TKV - 1 > q0))
-      softmax_tile<true, M>(s, pk, m, corr, rescale, kv0, q0, g, c, L, p.causal, cs, thr);
+      softmax_tile<true, M>(s, pk, mref, lim, corr, rescale, kv0, q0, g, c, L, p.causal, cs, hook);
     else
-      softmax_tile<false, M>(s, pk, m, corr, rescale, kv0, q0, g, c, L, p.causal, cs, thr);
+      softmax_tile<false, M>(s, pk, mref, lim, corr, rescale, kv0, q0, g, c, L, p.causal, cs, hook);
   };
 
   // Phase schedule.  Step j of a wave is its matrix phase M(j) = GEMM2 of
@@ -541,8 +564,8 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   // a wave whose rows all precede a tile (causal) sees only masked keys
   // there and adds nothing, which keeps one straight path through the loop.
   //
-  // Every wave requests its part of tile j + 1 + AHEAD at the start of S(j)
-  // and waits for its copies of tile j + 2 at the end of it.  The requested
+  // Every wave requests its part of tile j + 1 + AHEAD during S(j) and
+  // waits for its copies of tile j + 2 at the end of it.  The requested
   // tile's stage held tile j + 1 + AHEAD - ST <= j - 2, whose V tile was
   // last read in M(j - 1), which both groups have finished when either
   // starts S(j); tile j + 2 is first read in M(j + 2), after the barriers
@@ -550,16 +573,15 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   if (n > 0) {
     // Tiles 0 and 1 are needed first; the next ones follow once they have
     // landed, so that no more than AHEAD tiles' copies are ever outstanding.
-    issue(0);
+    issue(0, 0, NC);
     if constexpr (4 * LPW > 63) wait_vmcnt<0>();
-    if (1 < n) issue(1);
+    if (1 < n) issue(1, 0, NC);
     wait_vmcnt<0>();
-    for (int j = 2; j <= AHEAD && j < n; ++j) issue(j);
+    for (int j = 2; j <= AHEAD && j < n; ++j) issue(j, 0, NC);
     lds_barrier();
     if (grp == 1) lds_barrier();
     auto vector_phase = [&](int j) ATTN_INLINE {
-      if (j + 1 + AHEAD < n) issue(j + 1 + AHEAD);
-      sphase(j);
+      sphase(j, j + 1 + AHEAD);
       if (j + 2 < n) wait_tile(j + 2, min(n - 1, j + 1 + AHEAD));
       lds_barrier();
     };
@@ -586,7 +608,8 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   }
 
   // Epilogue.  Each of the four lane groups holds a partial row sum over its
-  // key subset (same reference max), so the total is their sum.
+  // key subset (same reference), so the total is their sum.  A split leaves
+  // its reference (base 2, -inf for a row that saw no key) beside the sum.
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const float lt = lacc[qb][0];
@@ -611,7 +634,8 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
       float* po = p.part_o + prow * D;
 #pragma unroll
       for (int db = 0; db < NDB; ++db) *reinterpret_cast<f32x4_t*>(po + 16 * db + 4 * g) = o[qb][db];
-      if (g == 0) *reinterpret_cast<float2*>(p.part_ml + prow * 2) = make_float2(m[qb], lt);
+      if (g == 0)
+        *reinterpret_cast<float2*>(p.part_ml + prow * 2) = make_float2(lim[qb] == -INFINITY ? -INFINITY : mref[qb], lt);
     }
   }
 }
