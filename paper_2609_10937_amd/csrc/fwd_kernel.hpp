@@ -38,7 +38,7 @@
 // the two run one phase apart (ping-pong): while one issues matrix products
 // the other issues the exponentials, which is the overlap a single wave
 // cannot get because its own vector work waits for its products.  Every
-// phase ends with a workgroup barrier; the operand reads of a matrix phase
+// step ends with a workgroup barrier; the operand reads of a matrix phase
 // are software-pipelined PF fragments ahead of the products that use them.
 //
 // Softmax bookkeeping keeps a per-row reference max m that is only raised
@@ -144,15 +144,6 @@ __device__ __forceinline__ void copy_to_lds(const void* base, uint32_t off, uint
                "s"(__builtin_amdgcn_readfirstlane(lds_dst))
                : "memory", "m0");
 }
-// The same copy for the tile that crosses the end of the sequence (per-lane
-// clamped offsets).  A distinct instruction string keeps the compiler from
-// merging the two paths into one with selects on every copy.
-__device__ __forceinline__ void copy_to_lds_edge(const void* base, uint32_t off, uint32_t lds_dst) {
-  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1 ; edge tile" ::"v"(off),
-               "s"(uniform_ptr(base)), "s"(__builtin_amdgcn_readfirstlane(lds_dst))
-               : "memory", "m0");
-}
-
 // Workgroup barrier that orders LDS accesses but leaves in-flight
 // global->LDS copies alone (the compiler's __syncthreads would drain them).
 __device__ __forceinline__ void lds_barrier() {
@@ -197,25 +188,44 @@ __device__ __forceinline__ int v_swz(int r) {
 // second product.  The row sums are formed by the second product itself (a
 // block of ones times the packed weights), so they add exactly the 16-bit
 // weights that multiply V.  MASK = true for tiles crossing the causal
-// diagonal or the end of the sequence.  hook(qb) runs before row block qb
-// (the vector phase spreads its tile copies over the softmax with it).
-template <bool MASK, typename M, int NKB, int NP, int QB, typename Hook>
+// diagonal or the end of the sequence.
+// Maximum of N values as a tree of 3-way maxima (v_max3_f32): depth
+// log3 N instead of a chain of N/2 dependent operations.
+template <int N>
+__device__ __forceinline__ float tree_max(const float* t) {
+  if constexpr (N == 1) {
+    return t[0];
+  } else if constexpr (N == 2) {
+    return fmaxf(t[0], t[1]);
+  } else {
+    constexpr int K = (N + 2) / 3;
+    float u[K];
+#pragma unroll
+    for (int i = 0; i < N / 3; ++i) u[i] = fmaxf(fmaxf(t[3 * i], t[3 * i + 1]), t[3 * i + 2]);
+    if constexpr (N % 3 == 2) u[N / 3] = fmaxf(t[N - 2], t[N - 1]);
+    if constexpr (N % 3 == 1) u[N / 3] = t[N - 1];
+    return tree_max<K>(u);
+  }
+}
+
+template <bool MASK, typename M, int NKB, int NP, int QB>
 __device__ __forceinline__ void softmax_tile(f32x4_t (&s)[NKB][QB], typename M::V8 (&pk)[NP][QB], float (&mref)[QB],
                                              float (&lim)[QB], float (&corr)[QB], bool& rescale, int kv0, int q0,
-                                             int g, int c, int L, int causal, float cs, Hook&& hook) {
+                                             int g, int c, int L, int causal, float cs) {
   using V2 = typename M::V2;
   using S = typename M::S;
+  // Scores of all row blocks first (independent work for the scheduler),
+  // then one check for the whole tile.
+  float mx[QB];
+  bool hit = false;
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
-    __builtin_amdgcn_sched_barrier(0);
-    hook(qb);
-    __builtin_amdgcn_sched_barrier(0);
-    const int q = q0 + 16 * qb + c;
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
       for (int r = 0; r < 4; ++r) s[kb][qb][r] = __builtin_fmaf(s[kb][qb][r], cs, -mref[qb]);
     if constexpr (MASK) {
+      const int q = q0 + 16 * qb + c;
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
@@ -224,18 +234,21 @@ __device__ __forceinline__ void softmax_tile(f32x4_t (&s)[NKB][QB], typename M::
           if (!(kv < L && !(causal && kv > q))) s[kb][qb][r] = -INFINITY;
         }
     }
-    float mx = s[0][qb][0];
+    float t[4 * NKB];
 #pragma unroll
-    for (int kb = 0; kb < NKB; ++kb)
+    for (int i = 0; i < 4 * NKB; ++i) t[i] = s[i >> 2][qb][i & 3];
+    mx[qb] = tree_max<4 * NKB>(t);
+    hit |= mx[qb] > lim[qb];
+  }
+  if (__any(hit)) {
 #pragma unroll
-      for (int r = (kb == 0 ? 1 : 0); r < 4; r += 2)
-        mx = (r + 1 < 4) ? fmaxf(mx, fmaxf(s[kb][qb][r], s[kb][qb][r + 1])) : fmaxf(mx, s[kb][qb][r]);
-    if (__any(mx > lim[qb])) {
-      mx = max_across_rows(mx);
+    for (int qb = 0; qb < QB; ++qb) {
+      if (!__any(mx[qb] > lim[qb])) continue;
+      const float rmx = max_across_rows(mx[qb]);
       const bool has = lim[qb] != -INFINITY;
       // New reference: the row maximum if above the old one; a row without
       // a reference takes its maximum as is (nothing has been accumulated).
-      const float delta = has ? fmaxf(mx, 0.f) : (mx == -INFINITY ? 0.f : mx);
+      const float delta = has ? fmaxf(rmx, 0.f) : (rmx == -INFINITY ? 0.f : rmx);
       if (__any(delta != 0.f)) {
         corr[qb] = has ? exp2_hw(-delta) : 0.f;
         mref[qb] += delta;
@@ -243,8 +256,11 @@ __device__ __forceinline__ void softmax_tile(f32x4_t (&s)[NKB][QB], typename M::
         for (int kb = 0; kb < NKB; ++kb) s[kb][qb] -= delta;
         rescale = true;
       }
-      if (mx != -INFINITY) lim[qb] = 8.f;
+      if (rmx != -INFINITY) lim[qb] = 8.f;
     }
+  }
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
     for (int pp = 0; pp < NP; ++pp) {
       uint32_t wd[4];
@@ -258,7 +274,12 @@ __device__ __forceinline__ void softmax_tile(f32x4_t (&s)[NKB][QB], typename M::
         }
       pk[pp][qb] = __builtin_bit_cast(typename M::V8, (u32x4_t){wd[0], wd[1], wd[2], wd[3]});
     }
-  }
+  // The weights are complete here: without this the compiler may sink the
+  // exponentials past the end-of-step barrier, next to their first use.
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+    for (int pp = 0; pp < NP; ++pp) asm volatile("" : "+v"(pk[pp][qb]));
 }
 
 template <int DT, int D, int TKV, int QB, int NW, int ST>
@@ -279,13 +300,15 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   constexpr int LPW = CHUNKS / (NCW * 64);  // 1 KB copies per copying wave per tile and tensor
   static_assert(TKV % 32 == 0 && D % 32 == 0 && KCH >= 8 && (KCH & (KCH - 1)) == 0, "tile alignment");
   static_assert(CHUNKS % (NCW * 64) == 0, "tile copies must split evenly across waves");
-  // Tiles requested ahead.  In S(j) a wave requests its part of
-  // tile j + 1 + AHEAD, whose stage held tile j + 1 + AHEAD - ST; that V tile
-  // must have been read by both groups, i.e. in M(j - 1) at the latest,
-  // which allows ST - 3.  The 6-bit vector-memory counter (at most AHEAD
-  // tiles of 2 LPW copies outstanding) allows 63 / (2 LPW).
-  constexpr int AHEAD = (ST - 3) < 63 / (2 * LPW) ? (ST - 3) : 63 / (2 * LPW);
-  static_assert(ST >= 3 && AHEAD >= 1, "stages");
+  // Tiles requested ahead.  In M(j) a wave requests its part of tile
+  // j + 1 + AHEAD, whose stage held tile j + 1 + AHEAD - ST; that V tile is
+  // read in M(j + 2 + AHEAD - ST), which every wave must have finished: all
+  // have finished M(j - 1) at the barrier before M(j), and the other group
+  // may be in M(j) itself, reading tiles j and j - 1; both allow ST - 3.  A
+  // wave has at most AHEAD + 1 tiles of 2 LPW copies outstanding, and the
+  // 6-bit vector-memory counter holds 63.
+  constexpr int AHEAD = (ST - 3) < 63 / (2 * LPW) - 1 ? (ST - 3) : 63 / (2 * LPW) - 1;
+  static_assert(ST >= 3 && AHEAD >= 0, "stages");
   constexpr int NVF = NP * NDB;             // V^T fragments per tile (GEMM2 A operands)
   constexpr int NKF = KC * NKB;             // K fragments per tile (GEMM1 A operands)
   constexpr int PF = 6;                     // operand fragments loaded ahead of their use
@@ -299,7 +322,7 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   const int c = lane & 15;
   const int L = p.L;
   // Waves w and w + 4 of a workgroup share a SIMD.  With two waves per SIMD
-  // the second runs one workgroup phase behind the first, so that one issues
+  // the second runs half a step behind the first, so that one issues
   // matrix products while the other runs the softmax.
   const int grp = NW == 8 ? (w >> 2) : 0;
 
@@ -339,57 +362,43 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
 
   // Copy tile j (relative to t_begin) of K and V into stage j % ST: the
   // copying wave's LPW 1 KB blocks of each tile image.  Image slot P holds
-  // row P/KCH, logical chunk (P%KCH) ^ swizzle(row).  The byte offsets of a
-  // lane's sources within a tile are fixed, so each copy is a wave-uniform
-  // tile base plus a 32-bit lane offset.  In the tile that crosses the end
-  // of the sequence, rows past the end are clamped to row L-1 (finite data
-  // that the mask removes).
-  // Block b of a tile image (1 KB) holds rows b*RPB .. b*RPB + RPB - 1.  A
-  // copying wave cw takes blocks cw, cw + NCW, cw + 2 NCW, ...; when NCW * RPB is
-  // a multiple of 16 rows (the period of both swizzles) its lanes' source
-  // offsets differ between those blocks by a constant, so one offset per
-  // tensor serves all of them.
+  // row P/KCH, logical chunk (P%KCH) ^ swizzle(row).  Block b of a tile image
+  // (1 KB) holds rows b*RPB .. b*RPB + RPB - 1; copying wave cw takes blocks
+  // cw, cw + NCW, cw + 2 NCW, ..., so block i of a lane sits at row
+  // r0 + i NCW RPB.  Each copy is the head's base address (wave-uniform) plus
+  // a lane offset: source row min(kv0 + row, L - 1) -- rows past the end of
+  // the sequence repeat row L-1 (finite data that the mask removes), so every
+  // tile, and every tile index, takes the same branch-free path -- and the
+  // byte offset of the lane's chunk within the row.  When NCW * RPB is a
+  // multiple of 16 rows (the period of both swizzles) the chunk offsets of
+  // all of a lane's blocks coincide.
   constexpr int RPB = 1024 / ROWB;
   constexpr bool SHIFT = (NCW * RPB) % 16 == 0;
+  constexpr int NCB = SHIFT ? 1 : LPW;
   const int cw = w;  // index among the copying waves
-  uint32_t koff[SHIFT ? 1 : LPW], voff[SHIFT ? 1 : LPW];
+  const uint32_t r0 = (uint32_t)((cw * 64 + lane) / KCH);
+  uint32_t kcb[NCB], vcb[NCB];
 #pragma unroll
-  for (int i = 0; i < (SHIFT ? 1 : LPW); ++i) {
-    const int P = (i * NCW + cw) * 64 + lane;
-    const int r = P / KCH, pc = P % KCH;
-    koff[i] = (uint32_t)(r * ROWB + ((pc ^ k_swz<KCH>(r)) * 16));
-    voff[i] = (uint32_t)(r * ROWB + ((pc ^ v_swz<KCH>(r)) * 16));
+  for (int i = 0; i < NCB; ++i) {
+    const int r = (int)r0 + i * NCW * RPB, pc = lane % KCH;
+    kcb[i] = (uint32_t)((pc ^ k_swz<KCH>(r)) * 16);
+    vcb[i] = (uint32_t)((pc ^ v_swz<KCH>(r)) * 16);
   }
-  auto ko = [&](int i) ATTN_INLINE { return SHIFT ? koff[0] + (uint32_t)(i * NCW * 1024) : koff[SHIFT ? 0 : i]; };
-  auto vo = [&](int i) ATTN_INLINE { return SHIFT ? voff[0] + (uint32_t)(i * NCW * 1024) : voff[SHIFT ? 0 : i]; };
   // This wave's part of tile j: its LPW blocks of the K image and of the V
   // image, as copies 0 .. NC-1 (copy 2i is block i of K, 2i+1 block i of V);
-  // issue(j, lo, hi) makes copies lo .. hi-1.  With SHIFT the per-block
-  // source offsets differ by a constant, added to the wave-uniform base
-  // instead of the lane offset.
+  // issue(j, lo, hi) makes copies lo .. hi-1.
   constexpr int NC = 2 * LPW;
+  static_assert((unsigned long long)ATTN_MAX_L * ROWB <= (1ull << 32), "32-bit lane offsets reach every row");
   auto issue = [&](int j, int lo, int hi) ATTN_INLINE {
-    const int kv0 = (t_begin + j) * TKV;
+    const uint32_t kv0 = (uint32_t)((t_begin + j) * TKV);
     const uint32_t kdst = (uint32_t)__builtin_amdgcn_readfirstlane(lds0 + (j % ST) * STAGEB) + cw * 1024;
-    const char* ksrc = reinterpret_cast<const char*>(Kh) + (size_t)kv0 * ROWB;
-    const char* vsrc = reinterpret_cast<const char*>(Vh) + (size_t)kv0 * ROWB;
-    if (kv0 + TKV <= L) {
+    const uint32_t t = kv0 + r0;
 #pragma unroll
-      for (int ci = lo; ci < hi; ++ci) {
-        const int i = ci >> 1;
-        const int step = SHIFT ? i * NCW * 1024 : 0;
-        if (ci & 1) copy_to_lds(vsrc + step, SHIFT ? voff[0] : voff[SHIFT ? 0 : i], kdst + TILEB + i * NCW * 1024);
-        else copy_to_lds(ksrc + step, SHIFT ? koff[0] : koff[SHIFT ? 0 : i], kdst + i * NCW * 1024);
-      }
-    } else {
-#pragma unroll
-      for (int ci = lo; ci < hi; ++ci) {
-        const int i = ci >> 1;
-        const int r = ((i * NCW + cw) * 64 + lane) / KCH;
-        const uint32_t back = (uint32_t)(max(0, kv0 + r - (L - 1)) * ROWB);  // bytes back to row L-1
-        if (ci & 1) copy_to_lds_edge(vsrc, vo(i) - back, kdst + TILEB + i * NCW * 1024);
-        else copy_to_lds_edge(ksrc, ko(i) - back, kdst + i * NCW * 1024);
-      }
+    for (int ci = lo; ci < hi; ++ci) {
+      const int i = ci >> 1;
+      const uint32_t row = min(t + (uint32_t)(i * NCW * RPB), (uint32_t)(L - 1));
+      if (ci & 1) copy_to_lds(Vh, row * ROWB + vcb[SHIFT ? 0 : i], kdst + TILEB + i * NCW * 1024);
+      else copy_to_lds(Kh, row * ROWB + kcb[SHIFT ? 0 : i], kdst + i * NCW * 1024);
     }
   };
   // This wave's copies of tile j are complete once no more than the copies
@@ -405,6 +414,10 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
 
   const float cs = p.c;  // scale * log2(e): scores in the base-2 domain
 
+  // Prologue copies: tile 0, then the Q loads, then tiles 1 .. AHEAD, so
+  // that the Q loads and the first tile travel together; both are complete
+  // once only the later tiles' copies are outstanding.
+  if (n > 0) issue(0, 0, NC);
   // Q fragments: B operand of S^T = K Q^T, one 16-byte load per (block, k step).
   V8 qf[QB][KC];
 #pragma unroll
@@ -417,8 +430,13 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
       qf[qb][kc] = __builtin_bit_cast(V8, x);
     }
   }
-  // Drain the Q loads here: the loop's waits count only tile copies.
-  wait_vmcnt<0>();
+  if (n > 0) {
+#pragma unroll
+    for (int j = 1; j <= AHEAD; ++j) issue(j, 0, NC);
+    wait_tile(0, AHEAD);
+  } else {
+    wait_vmcnt<0>();
+  }
 
   f32x4_t o[QB][NDB];
   f32x4_t lacc[QB];  // row sums of the weights (all four entries of a lane equal)
@@ -475,7 +493,13 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   // The stage offsets pass through readfirstlane: as opaque wave-uniform
   // values they stay one scalar add per phase instead of becoming one
   // induction variable per fragment address.
-  auto mphase = [&](auto g2c, auto g1c, int j) ATTN_INLINE {
+  // The phase also carries this wave's copies of tile jc, spread over the
+  // products: the products keep the matrix core busy while a copy waits for
+  // the address unit, and the copies of the workgroup's waves do not all
+  // queue at once.  Tiles past the range are copied too (in-bounds rows, into
+  // stages no later phase reads), which keeps the phase one basic block and
+  // the copy count per step constant.
+  auto mphase = [&](auto g2c, auto g1c, int j, int jc) ATTN_INLINE {
     constexpr bool G2 = decltype(g2c)::value, G1 = decltype(g1c)::value;
     constexpr int F = (G2 ? NVF : 0) + (G1 ? NKF : 0);
     const uint32_t Vs = vbase + (uint32_t)__builtin_amdgcn_readfirstlane(lds0 + ((j + ST - 1) % ST) * STAGEB + TILEB);
@@ -521,6 +545,11 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
           s[kb][qb] = M::run(buf[f], qf[qb][kc], kc == 0 ? (f32x4_t){0.f, 0.f, 0.f, 0.f} : s[kb][qb]);
       }
       if (f + PF < F) buf[f + PF] = load(f + PF);
+      if constexpr (G1) {
+#pragma unroll
+        for (int ci = 0; ci < NC; ++ci)
+          if (f == (2 * ci + 1) * F / (2 * NC)) issue(jc, ci, ci + 1);
+      }
     }
     // Keep that order through instruction scheduling: the first PF
     // fragments' reads, then per fragment its QB products and the reads of
@@ -541,70 +570,57 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
 
   // Vector phase S(j): the softmax of tile j.  Only tiles that cross the
   // causal diagonal or the end of the sequence take the masked body.
-  // Its hook spreads this wave's copies of tile jc over the row blocks, so
-  // that the copies of the workgroup's waves do not all queue at once.
-  auto sphase = [&](int j, int jc) ATTN_INLINE {
+  auto sphase = [&](int j) ATTN_INLINE {
     const int kv0 = (t_begin + j) * TKV;
-    auto hook = [&](int qb) ATTN_INLINE {
-      constexpr int per = NC % QB == 0 ? NC / QB : NC;
-      if (jc < n && qb * per < NC) issue(jc, qb * per, qb * per + per);
-    };
     if ((kv0 + TKV > L) || (p.causal && kv0 + TKV - 1 > q0))
-      softmax_tile<true, M>(s, pk, mref, lim, corr, rescale, kv0, q0, g, c, L, p.causal, cs, hook);
+      softmax_tile<true, M>(s, pk, mref, lim, corr, rescale, kv0, q0, g, c, L, p.causal, cs);
     else
-      softmax_tile<false, M>(s, pk, mref, lim, corr, rescale, kv0, q0, g, c, L, p.causal, cs, hook);
+      softmax_tile<false, M>(s, pk, mref, lim, corr, rescale, kv0, q0, g, c, L, p.causal, cs);
   };
 
-  // Phase schedule.  Step j of a wave is its matrix phase M(j) = GEMM2 of
-  // tile j-1 and GEMM1 of tile j, then its vector phase S(j); each phase
-  // ends with a workgroup barrier.  Group 1 starts one phase later than
-  // group 0 (an idle first phase) and group 0 ends with an idle phase, so
-  // both pass 2n + 4 barriers and the two waves of a SIMD are always in
-  // different kinds of phase.  Every wave computes every tile of the range:
-  // a wave whose rows all precede a tile (causal) sees only masked keys
-  // there and adds nothing, which keeps one straight path through the loop.
+  // Phase schedule.  M(j) is the matrix phase of tile j (GEMM2 of tile j-1
+  // and GEMM1 of tile j), S(j) its vector phase.  One workgroup barrier per
+  // step: between barriers B(j) and B(j+1) group 0 runs M(j) then S(j) and
+  // group 1 runs S(j-1) then M(j), so the two waves of a SIMD start each
+  // step in different kinds of phase (the matrix phase at raised priority)
+  // and drift back into step at every barrier.  Every wave computes every
+  // tile of the range: a wave whose rows all precede a tile (causal) sees
+  // only masked keys there and adds nothing, which keeps one straight path
+  // through the loop.
   //
-  // Every wave requests its part of tile j + 1 + AHEAD during S(j) and
-  // waits for its copies of tile j + 2 at the end of it.  The requested
-  // tile's stage held tile j + 1 + AHEAD - ST <= j - 2, whose V tile was
-  // last read in M(j - 1), which both groups have finished when either
-  // starts S(j); tile j + 2 is first read in M(j + 2), after the barriers
-  // that end S(j) of both groups.
+  // Copies.  A wave requests its part of tile j + 1 + AHEAD during M(j) and
+  // has its part of tile j + 1 complete before B(j + 1); the barrier then
+  // publishes the whole tile to M(j + 1) of both groups.
   if (n > 0) {
-    // Tiles 0 and 1 are needed first; the next ones follow once they have
-    // landed, so that no more than AHEAD tiles' copies are ever outstanding.
-    issue(0, 0, NC);
-    if constexpr (4 * LPW > 63) wait_vmcnt<0>();
-    if (1 < n) issue(1, 0, NC);
-    wait_vmcnt<0>();
-    for (int j = 2; j <= AHEAD && j < n; ++j) issue(j, 0, NC);
-    lds_barrier();
-    if (grp == 1) lds_barrier();
-    auto vector_phase = [&](int j) ATTN_INLINE {
-      sphase(j, j + 1 + AHEAD);
-      if (j + 2 < n) wait_tile(j + 2, min(n - 1, j + 1 + AHEAD));
+    auto matrix = [&](auto g2c, auto g1c, int j) ATTN_INLINE {
+      __builtin_amdgcn_s_setprio(1);
+      mphase(g2c, g1c, j, j + 1 + AHEAD);
+      __builtin_amdgcn_s_setprio(0);
+    };
+    const std::false_type no{};
+    const std::true_type yes{};
+    lds_barrier();  // B(0)
+    // End of a wave's step j: its part of tile j + 1 complete, then the
+    // barrier.  Group 1's steps end after its matrix phases, group 0's after
+    // its vector phases; the phases themselves are one straight sequence.
+    auto end_step = [&](int j, int last_issued) ATTN_INLINE {
+      if (j + 1 < n) wait_tile(j + 1, last_issued);
       lds_barrier();
     };
-    // Step 0: GEMM1 of the first tile only.
-    __builtin_amdgcn_s_setprio(1);
-    mphase(std::false_type{}, std::true_type{}, 0);
-    __builtin_amdgcn_s_setprio(0);
-    lds_barrier();
-    vector_phase(0);
+    matrix(no, yes, 0);
+    if (grp == 1) end_step(0, 1 + AHEAD);
+    sphase(0);
+    if (grp == 0) end_step(0, 1 + AHEAD);
     for (int j = 1; j < n; ++j) {
-      __builtin_amdgcn_s_setprio(1);
-      mphase(std::true_type{}, std::true_type{}, j);
-      __builtin_amdgcn_s_setprio(0);
-      lds_barrier();
-      vector_phase(j);
+      matrix(yes, yes, j);
+      if (grp == 1) end_step(j, j + 1 + AHEAD);
+      sphase(j);
+      if (grp == 0) end_step(j, j + 1 + AHEAD);
     }
-    // Step n: GEMM2 of the last tile, then an idle vector phase.
-    __builtin_amdgcn_s_setprio(1);
-    mphase(std::true_type{}, std::false_type{}, n);
-    __builtin_amdgcn_s_setprio(0);
-    lds_barrier();
-    lds_barrier();
-    if (grp == 0) lds_barrier();
+    matrix(yes, no, n);
+    // The copies of the tiles past the range land before the workgroup's
+    // LDS is released.
+    wait_vmcnt<0>();
   }
 
   // Epilogue.  Each of the four lane groups holds a partial row sum over its
