@@ -142,8 +142,10 @@ def sampled_parity(w, q, k, v, out):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    # Sustained work raises the GPU clock over the first few milliseconds;
+    # 50 steps (about 7 ms of kernel time) bring it to its steady level.
+    ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle timing")
     ap.add_argument("--no-secondary", action="store_true", help="skip the batched causal workload")
     ap.add_argument("--no-unfused", action="store_true", help="skip the unfused baseline")

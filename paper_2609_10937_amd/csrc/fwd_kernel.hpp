@@ -311,7 +311,7 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   static_assert(ST >= 3 && AHEAD >= 0, "stages");
   constexpr int NVF = NP * NDB;             // V^T fragments per tile (GEMM2 A operands)
   constexpr int NKF = KC * NKB;             // K fragments per tile (GEMM1 A operands)
-  constexpr int PF = 6;                     // operand fragments loaded ahead of their use
+  constexpr int PF = 4;                     // operand fragments loaded ahead of their use
 
   __shared__ __attribute__((aligned(1024))) uint16_t smem[ST * 2 * TILE];
 
