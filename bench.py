@@ -71,31 +71,31 @@ def time_steps(fn, steps, warmup):
 
 
 def cpu_baseline(w, q, k, v):
-    """The oracle (float32 variant, untouched) on the host cores over a bounded
-    sample of the same workload: every key, a contiguous block of query rows."""
+    """The oracle as it stands (float64) on the host cores over a bounded sample
+    of the same workload: every key, a contiguous block of query rows."""
     from oracle import attention as A
     try:
         from threadpoolctl import threadpool_info
         cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     except Exception:
         cores = len(os.sched_getaffinity(0))
-    qh = inputs.bits_to_f32(q[0, 0], w.dtype)
-    kh = inputs.bits_to_f32(k[0, 0], w.dtype)
-    vh = inputs.bits_to_f32(v[0, 0], w.dtype)
+    qh = inputs.bits_to_f64(q[0, 0], w.dtype)
+    kh = inputs.bits_to_f64(k[0, 0], w.dtype)
+    vh = inputs.bits_to_f64(v[0, 0], w.dtype)
+    A.attention_head(qh, kh, vh, w.scale, w.causal, rows=np.arange(256))  # untimed: thread pools, first touch
+    # grow the sample until it is several seconds of work (bounded by the full head)
     rows = 1024
-    t0 = time.perf_counter()
-    A.attention_head(qh, kh, vh, w.scale, w.causal, rows=np.arange(rows), dtype=np.float32)
-    dt = time.perf_counter() - t0
-    # grow the sample until it is about ten seconds of work (bounded by the full head)
-    if dt < 2.0:
-        rows = int(min(w.L, rows * max(1.0, 10.0 / max(dt, 1e-3))))
-        rows = max(1024, rows - rows % 512)
+    while True:
         t0 = time.perf_counter()
-        A.attention_head(qh, kh, vh, w.scale, w.causal, rows=np.arange(rows), dtype=np.float32)
+        A.attention_head(qh, kh, vh, w.scale, w.causal, rows=np.arange(rows))
         dt = time.perf_counter() - t0
+        if dt >= 5.0 or rows >= w.L:
+            break
+        rows = int(min(w.L, rows * max(2.0, 10.0 / max(dt, 1e-3))))
+        rows = max(1024, rows - rows % 512)
     fl = 4.0 * rows * w.L * w.d
     return {"value": fl / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"float32 oracle, query rows 0..{rows - 1} of {w.L} against all {w.L} keys "
+            "sample": f"float64 oracle, query rows 0..{rows - 1} of {w.L} against all {w.L} keys "
                       f"(B=1, H=1, d={w.d}), {dt:.2f} s"}
 
 
