@@ -326,13 +326,32 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   // matrix products while the other runs the softmax.
   const int grp = NW == 8 ? (w >> 2) : 0;
 
-  // Workgroup -> (query tile, head, split).  Heads vary fastest among
-  // workgroups of one query-tile rank; causal launches heavy tiles first.
-  const int per_rank = p.BH * p.n_split;
-  const int rank = blockIdx.x / per_rank;
-  const int rem = blockIdx.x - rank * per_rank;
-  const int head = rem / p.n_split;
-  const int split = rem - head * p.n_split;
+  // Workgroup -> (query tile, head, split).  A unit is one (head, split)
+  // pair: its n_qt query tiles all read the same key range.  Workgroups are
+  // dispatched to the 8 XCDs round-robin (block b on XCD b % 8), each XCD with
+  // its own L2, so when the units divide evenly XCD x takes units x, x + 8, ...
+  // and runs them xg at a time, ranks outermost within such a group: the
+  // workgroups an XCD runs together then stream the same K/V tiles through
+  // its L2.  A group holds at least 64 query tiles (two per CU of an XCD) so
+  // that heavy and light causal tiles still balance.  Causal launches heavy
+  // tiles (high ranks of the query order) first.  Otherwise the plain order:
+  // units fastest within a rank.
+  const int units = p.BH * p.n_split;
+  int xg = 1;
+  while (xg * p.n_qt < 64) xg *= 2;
+  int unit, rank;
+  if (units % (8 * xg) == 0) {
+    const int x = blockIdx.x % 8, i = blockIdx.x / 8;
+    const int per_group = xg * p.n_qt;
+    const int gi = i / per_group, r = i - gi * per_group;
+    rank = r / xg;
+    unit = x + 8 * (gi * xg + (r - rank * xg));
+  } else {
+    rank = blockIdx.x / units;
+    unit = blockIdx.x - rank * units;
+  }
+  const int head = unit / p.n_split;
+  const int split = unit - head * p.n_split;
   const int qt = p.causal ? (p.n_qt - 1 - rank) : rank;
 
   const size_t hoff = (size_t)head * (size_t)L * D;
