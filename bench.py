@@ -149,6 +149,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle timing")
     ap.add_argument("--no-secondary", action="store_true", help="skip the batched causal workload")
     ap.add_argument("--no-unfused", action="store_true", help="skip the unfused baseline")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the sequence-length sweep (Table 3)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="finish with two plain 256 MiB device copies (reference for byte counters)")
     args = ap.parse_args()
@@ -221,6 +222,30 @@ def main():
         del t2, o2
         torch.cuda.empty_cache()
 
+    sweep = None
+    if not args.no_sweep:
+        # Table 3: fused vs unfused over L at d=128, one head.  The paper's
+        # speedups (its fp32 GPU) ride along as context.
+        paper_speedup = {4096: 0.95, 8192: 1.25, 16384: 1.50, 32768: 1.68}
+        sweep = []
+        for ws_w in inputs.SWEEP:
+            print(f"bench: sweep L={ws_w.L}", file=sys.stderr, flush=True)
+            ts = [upload(x, ws_w.dtype) for x in inputs.workload_inputs(ws_w)]
+            tos = torch.empty_like(ts[0])
+            _, f_ms = time_steps(lambda: capi.attn_fwd(ts[0], ts[1], ts[2], tos, ws_w.scale, ws_w.causal), 20, 20)
+            wsu = torch.empty(capi.attn_unfused_workspace_bytes(1, 1, ws_w.L, capi.ATTN_BF16), dtype=torch.uint8,
+                              device="cuda")
+            _, u_ms = time_steps(lambda: capi.attn_fwd_unfused(ts[0], ts[1], ts[2], tos, ws_w.scale, ws_w.causal,
+                                                               wsu), 5, 2)
+            fl_s = flops(ws_w)
+            sweep.append({"L": ws_w.L, "fused_ms": round(f_ms, 4), "unfused_ms": round(u_ms, 4),
+                          "speedup": round(u_ms / f_ms, 2), "paper_speedup": paper_speedup.get(ws_w.L),
+                          "fused_tflops": round(fl_s / (f_ms * 1e-3) / 1e12, 1),
+                          "fused_pct_peak": round(100 * fl_s / (f_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 1),
+                          "fused_bytes": fused_bytes(ws_w), "unfused_bytes": unfused_bytes(ws_w)})
+            del ts, tos, wsu
+            torch.cuda.empty_cache()
+
     cpu = None
     if not args.no_cpu:
         print("bench: cpu oracle", file=sys.stderr, flush=True)
@@ -262,6 +287,7 @@ def main():
             "hbm_rate_tbps": round(unfused_bytes(w) / (u_ev * 1e-3) / 1e12, 3)},
         "parity": parity,
         "secondary": secondary,
+        "l_sweep": sweep,
         "cpu_baseline": cpu,
     }
     if args.copy_calibration:

@@ -53,6 +53,17 @@ WORKLOADS = {
 }
 
 
+# The sequence-length sweep of the paper's Table 3 (single head, d=128,
+# non-causal); L=16384 is the headline workload itself.
+SWEEP = (
+    Workload("sweep_l4096_d128", 1, 1, 4096, 128, "bf16", False, 1.0, 1101),
+    Workload("sweep_l8192_d128", 1, 1, 8192, 128, "bf16", False, 1.0, 1102),
+    WORKLOADS["single_head_l16384_d128"],
+    Workload("sweep_l32768_d128", 1, 1, 32768, 128, "bf16", False, 1.0, 1104),
+)
+WORKLOADS.update({w.name: w for w in SWEEP})
+
+
 def softmax_scale(d: int) -> float:
     """1/sqrt(d) evaluated in float32, returned as the Python float of that value."""
     return float(np.float32(1.0) / np.sqrt(np.float32(d)))

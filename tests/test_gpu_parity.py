@@ -59,7 +59,8 @@ def test_paper_structured_layout_case(dtype):
 
 # ------------------------------------------------------------ named workloads
 
-SMALL = ["tiny_f16_l128_d64", "h8_l1024_d128", "causal_b2h16_l4096_d128_kx3", "single_head_l16384_d128"]
+SMALL = ["tiny_f16_l128_d64", "h8_l1024_d128", "causal_b2h16_l4096_d128_kx3", "single_head_l16384_d128",
+         "sweep_l4096_d128", "sweep_l8192_d128"]
 
 
 @pytest.mark.parametrize("name", SMALL)
@@ -100,6 +101,30 @@ def test_full_occupancy_causal_sampled_rows():
     vmin = -torch.cummax(-vf, dim=2).values
     slack = 2e-2
     assert (of <= vmax + slack).all() and (of >= vmin - slack).all()
+
+
+def test_sweep_l32768_sampled_rows():
+    """The longest point of the sequence-length sweep (B=H=1, L=32768, d=128):
+    sampled rows against the oracle, and every row inside the range of V."""
+    w = inputs.WORKLOADS["sweep_l32768_d128"]
+    print(f"case workload {w.name} (sampled)", flush=True)
+    q, k, v = inputs.workload_inputs(w)
+    tq, tk, tv = (_gpu.upload(x, w.dtype) for x in (q, k, v))
+    o = _gpu.fused(tq, tk, tv, w.scale, w.causal)
+    L = w.L
+    rows = np.unique(np.concatenate([np.arange(0, 40), np.arange(L - 40, L),
+                                     np.random.default_rng(78).integers(0, L, 160),
+                                     [255, 256, 257, 8191, 8192, 16383, 16384]]))
+    got = _gpu.download(o[0, 0, torch.from_numpy(rows).to("cuda")], w.dtype)
+    ref = A.attention_head(_f64(q[0, 0], w.dtype), _f64(k[0, 0], w.dtype), _f64(v[0, 0], w.dtype),
+                           w.scale, False, rows=rows)
+    mx, mn = _gpu.assert_close(got, ref, w.dtype, w.name)
+    print(f"  {w.name}: max_abs {mx:.3e} mean_abs {mn:.3e} over {rows.size} rows", flush=True)
+    of = o.float()[0, 0]
+    vf = tv.float()[0, 0]
+    assert torch.isfinite(of).all()
+    slack = 2e-2
+    assert (of <= vf.max(dim=0).values + slack).all() and (of >= vf.min(dim=0).values - slack).all()
 
 
 # ------------------------------------------------------------ edge shapes
