@@ -126,6 +126,24 @@ def measured_traffic(workload):
     return None if entry is None else entry.get("hbm_bytes_per_launch")
 
 
+def measured_mfma(workload):
+    """Matrix-core busy fraction and clock of the fused kernel from the committed
+    counter summary, if it was taken on the current kernel sources (else None)."""
+    path = os.path.join(ROOT, "profiles", "fwd_kernel_mfma_busy.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    e = rec.get("workloads", {}).get(workload)
+    if e is None:
+        return None
+    return {"busy_frac": e["mfma_busy_frac"], "clock_ghz": e["clock_ghz"],
+            "source": "profiles/fwd_kernel_mfma_busy.md"}
+
+
 def sampled_parity(w, q, k, v, out):
     from oracle import attention as A
     import torch
@@ -217,6 +235,7 @@ def main():
         secondary = {"workload": w2.name, "ms": round(ev2, 4),
                      "tflops": round(flops(w2) / (ev2 * 1e-3) / 1e12, 2),
                      "pct_peak": round(100 * flops(w2) / (ev2 * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
+                     "mfma_counters": measured_mfma(w2.name),
                      "tiles": {"t_kv": p2.t_kv, "t_q_wave": p2.t_q_wave, "n_waves": p2.n_waves,
                                "n_split": p2.n_split, "grid": p2.grid}}
         del t2, o2
@@ -277,6 +296,7 @@ def main():
                      "traffic": measured_traffic(w.name),
                      "kernel": "fwd_kernel (attn_fwd_partial), HIP events per launch",
                      "kernel_ms": round(k_ms, 5), "step_event_ms": round(ev_ms, 5),
+                     "mfma_counters": measured_mfma(w.name),
                      "algorithmic_flops_per_launch": fl, "algorithmic_bytes_per_launch": fused_bytes(w)},
         "hbm_bytes": {"fused_algorithmic": fused_bytes(w), "unfused_algorithmic": unfused_bytes(w),
                       "ratio": unfused_bytes(w) / fused_bytes(w)},
