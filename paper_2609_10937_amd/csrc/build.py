@@ -31,6 +31,8 @@ SOURCES = [
     "fwd_bf16_d128.hip",
     "fwd_f16_d64.hip",
     "fwd_f16_d128.hip",
+    "fwd_bf16_d256.hip",
+    "fwd_f16_d256.hip",
 ]
 
 ARCH = "gfx950"

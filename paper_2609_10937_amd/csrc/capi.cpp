@@ -15,6 +15,8 @@ const FwdInstance* fwd_instances_bf16_d64(int* n);
 const FwdInstance* fwd_instances_bf16_d128(int* n);
 const FwdInstance* fwd_instances_f16_d64(int* n);
 const FwdInstance* fwd_instances_f16_d128(int* n);
+const FwdInstance* fwd_instances_bf16_d256(int* n);
+const FwdInstance* fwd_instances_f16_d256(int* n);
 }  // namespace attn
 
 using namespace attn;
@@ -36,7 +38,8 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 int check_shape(int B, int H, int L, int d, int dtype) {
   if (B <= 0 || H <= 0 || L <= 0 || L > ATTN_MAX_L) return ATTN_E_SHAPE;
-  if (d != 64 && d != 128) return ATTN_E_UNSUPPORTED_D;
+  if (d != 64 && d != 128 && d != 256) return ATTN_E_UNSUPPORTED_D;
+  if ((int64_t)L * d * 2 > (int64_t(1) << 32)) return ATTN_E_SHAPE;  // byte offsets within a head are 32-bit
   if (dtype != ATTN_BF16 && dtype != ATTN_F16) return ATTN_E_DTYPE;
   const long double elems = (long double)B * H * L * d;
   if (elems >= 4.6e18L) return ATTN_E_SHAPE;
@@ -93,7 +96,8 @@ std::map<int, DeviceState> g_dev;
 
 const FwdInstance* find_instance(int dtype, int d, int t_kv, int q_blocks, int n_waves) {
   using Fn = const FwdInstance* (*)(int*);
-  Fn fns[] = {fwd_instances_bf16_d64, fwd_instances_bf16_d128, fwd_instances_f16_d64, fwd_instances_f16_d128};
+  Fn fns[] = {fwd_instances_bf16_d64, fwd_instances_bf16_d128, fwd_instances_bf16_d256,
+              fwd_instances_f16_d64,  fwd_instances_f16_d128,  fwd_instances_f16_d256};
   for (Fn f : fns) {
     int n = 0;
     const FwdInstance* t = f(&n);

@@ -44,10 +44,12 @@ hipError_t launch_combine(const FwdParams& p, int d, int dtype, hipStream_t s) {
   const int64_t threads = (int64_t)p.BH * p.L * (d / 4);
   const unsigned grid = (unsigned)((threads + 255) / 256);
   if (dtype == ATTN_BF16) {
-    if (d == 128) hipLaunchKernelGGL((combine_kernel<ATTN_BF16, 128>), dim3(grid), dim3(256), 0, s, p);
+    if (d == 256) hipLaunchKernelGGL((combine_kernel<ATTN_BF16, 256>), dim3(grid), dim3(256), 0, s, p);
+    else if (d == 128) hipLaunchKernelGGL((combine_kernel<ATTN_BF16, 128>), dim3(grid), dim3(256), 0, s, p);
     else hipLaunchKernelGGL((combine_kernel<ATTN_BF16, 64>), dim3(grid), dim3(256), 0, s, p);
   } else {
-    if (d == 128) hipLaunchKernelGGL((combine_kernel<ATTN_F16, 128>), dim3(grid), dim3(256), 0, s, p);
+    if (d == 256) hipLaunchKernelGGL((combine_kernel<ATTN_F16, 256>), dim3(grid), dim3(256), 0, s, p);
+    else if (d == 128) hipLaunchKernelGGL((combine_kernel<ATTN_F16, 128>), dim3(grid), dim3(256), 0, s, p);
     else hipLaunchKernelGGL((combine_kernel<ATTN_F16, 64>), dim3(grid), dim3(256), 0, s, p);
   }
   return hipGetLastError();

@@ -154,22 +154,27 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
-// 16-byte chunk swizzles of a row-major [rows][KCH chunks] tile (KCH = 16
-// for d = 128, 8 for d = 64), chosen so that every operand read of the
-// kernel hits distinct LDS banks:
+// 16-byte chunk swizzles of a row-major [rows][KCH chunks] tile (KCH = 32
+// for d = 256, 16 for d = 128, 8 for d = 64), chosen so that every operand
+// read of the kernel hits distinct LDS banks (64 banks of 4 bytes: a chunk's
+// bank group is its position modulo 16, and a 256-byte row of banks holds
+// 16 chunks):
 //  K (GEMM1 A operand, ds_read_b128): 16 lanes read 16 consecutive rows at
-//    one logical chunk -> distinct physical chunks across rows.
+//    one logical chunk -> distinct physical chunks modulo 16 across rows.
 //  V (GEMM2 A operand, ds_read_b64_tr_b16): a 32-lane pair of groups reads
 //    rows base + 0..3 and base + 4..7, two adjacent chunks each -> the row's
 //    low three bits select distinct chunk positions.
+// Rows of 32 chunks (two rows of banks) take the 16-chunk swizzles: only
+// the low four bits of the chunk index decide the bank group.
 template <int KCH>
 __device__ __forceinline__ int k_swz(int r) {
-  if constexpr (KCH == 16) return r & 15;
+  static_assert(KCH == 8 || KCH == 16 || KCH == 32, "chunks per row");
+  if constexpr (KCH >= 16) return r & 15;
   else return (r >> 1) & 7;
 }
 template <int KCH>
 __device__ __forceinline__ int v_swz(int r) {
-  if constexpr (KCH == 16) return (2 * (r & 3)) | (8 * ((r >> 2) & 1));
+  if constexpr (KCH >= 16) return (2 * (r & 3)) | (8 * ((r >> 2) & 1));
   else return 2 * ((r >> 1) & 3);
 }
 
@@ -407,7 +412,7 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   // image, as copies 0 .. NC-1 (copy 2i is block i of K, 2i+1 block i of V);
   // issue(j, lo, hi) makes copies lo .. hi-1.
   constexpr int NC = 2 * LPW;
-  static_assert((unsigned long long)ATTN_MAX_L * ROWB <= (1ull << 32), "32-bit lane offsets reach every row");
+  // 32-bit lane offsets reach every row: the host admits L * d * 2 <= 2^32.
   auto issue = [&](int j, int lo, int hi) ATTN_INLINE {
     const uint32_t kv0 = (uint32_t)((t_begin + j) * TKV);
     const uint32_t kdst = (uint32_t)__builtin_amdgcn_readfirstlane(lds0 + (j % ST) * STAGEB) + cw * 1024;

@@ -63,6 +63,14 @@ SWEEP = (
 )
 WORKLOADS.update({w.name: w for w in SWEEP})
 
+# Head dimension 256 (t_kv = 32, 16 rows per wave): one long head and a
+# batched causal case of the same flop count as the H=32, d=128 one.
+HEAD_DIM_256 = (
+    Workload("single_head_l16384_d256", 1, 1, 16384, 256, "bf16", False, 1.0, 1201),
+    Workload("causal_b4h16_l16384_d256", 4, 16, 16384, 256, "bf16", True, 1.0, 1202),
+)
+WORKLOADS.update({w.name: w for w in HEAD_DIM_256})
+
 
 def softmax_scale(d: int) -> float:
     """1/sqrt(d) evaluated in float32, returned as the Python float of that value."""

@@ -126,7 +126,7 @@ def test_fused_structure_plans_every_shape():
     """Every shape the API accepts maps to a compiled instance on the gfx950 descriptor."""
     hw = capi.attn_hw_desc_preset("gfx950")
     shapes = [(w.B, w.H, w.L, w.d, w.causal) for w in inputs.WORKLOADS.values()]
-    for d in (64, 128):
+    for d in (64, 128, 256):
         for L in (1, 2, 15, 16, 17, 31, 33, 63, 64, 65, 100, 127, 129, 159, 161, 1000, 1023, 4097,
                   16384, 65536, 1 << 20, capi.ATTN_MAX_L):
             for B, H in ((1, 1), (1, 3), (2, 8), (4, 32), (64, 64)):
@@ -135,13 +135,24 @@ def test_fused_structure_plans_every_shape():
     seen = set()
     for B, H, L, d, causal in shapes:
         for dt in (capi.ATTN_BF16, capi.ATTN_F16):
-            if B * H * L > (1 << 31) // 2:
+            if B * H * L > (1 << 31) // 2 or L * d * 2 > (1 << 32):
                 continue
             r = capi.attn_fwd_plan(B, H, L, d, causal, dt, hw=hw)
             assert r.feasible and r.grid >= 1
             assert r.vgpr_est <= r.vgpr_budget and r.lds_used <= r.lds_budget
             seen.add((d, r.t_kv, r.t_q_wave, r.n_waves))
-    assert (128, 64, 32, 8) in seen
+    assert (128, 64, 32, 8) in seen and (256, 32, 16, 8) in seen
+
+
+def test_head_bytes_fit_32_bit_offsets():
+    """A head's Q, K or V must stay within 4 GiB (L d 2 <= 2^32): L = 2^23 is the
+    largest sequence at d = 256, while d = 128 reaches ATTN_MAX_L = 2^24."""
+    hw = capi.attn_hw_desc_preset("gfx950")
+    assert capi.attn_fwd_plan(1, 1, 1 << 23, 256, 0, capi.ATTN_BF16, hw=hw).feasible
+    assert capi.attn_fwd_plan(1, 1, capi.ATTN_MAX_L, 128, 0, capi.ATTN_BF16, hw=hw).feasible
+    with pytest.raises(capi.AttnError) as e:
+        capi.attn_fwd_plan(1, 1, (1 << 23) + 1, 256, 0, capi.ATTN_BF16, hw=hw)
+    assert e.value.status == capi.CODE["ATTN_E_SHAPE"]
 
 
 def test_headline_plans():
@@ -229,7 +240,7 @@ def test_compiled_kernels_fit_without_scratch():
     with open(path) as f:
         res = json.load(f)
     fwd = {k: v for k, v in res.items() if "fwd_kernel" in k}
-    assert len(fwd) == 20
+    assert len(fwd) == 28
     for name, r in res.items():
         assert r["scratch"] == 0, name
     for name, r in fwd.items():

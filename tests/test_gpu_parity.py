@@ -129,7 +129,7 @@ def test_sweep_l32768_sampled_rows():
 
 # ------------------------------------------------------------ edge shapes
 
-EDGE = [(L, d, causal, dt) for L in (1, 17, 100, 1000, 4097) for d in (64, 128)
+EDGE = [(L, d, causal, dt) for L in (1, 17, 100, 1000, 4097) for d in (64, 128, 256)
         for causal in (False, True) for dt in ("bf16", "f16")]
 
 
@@ -142,6 +142,21 @@ def test_edge_shapes(L, d, causal, dtype):
     o = _gpu.fused(_gpu.upload(q, dtype), _gpu.upload(k, dtype), _gpu.upload(v, dtype), scale, causal)
     ref = A.attention(_f64(q, dtype), _f64(k, dtype), _f64(v, dtype), scale, causal)
     _gpu.assert_close(_gpu.download(o, dtype), ref, dtype, f"L{L} d{d} c{causal} {dtype}")
+
+
+@pytest.mark.parametrize("B,H,L,causal,dtype", [(1, 4, 2048, False, "bf16"), (2, 2, 3000, True, "f16"),
+                                                 (1, 1, 8192, False, "bf16")])
+def test_head_dim_256_all_rows(B, H, L, causal, dtype):
+    """d = 256 (t_kv = 32, 16 rows per wave): all rows against the oracle; the
+    single-head case runs with split key ranges, the L = 3000 case has a ragged
+    tail tile."""
+    print(f"case d256 B{B} H{H} L{L} causal{int(causal)} {dtype}", flush=True)
+    q, k, v = inputs.make_qkv(B, H, L, 256, dtype, seed=L + 256)
+    s = inputs.softmax_scale(256)
+    o = _gpu.fused(_gpu.upload(q, dtype), _gpu.upload(k, dtype), _gpu.upload(v, dtype), s, causal)
+    ref = A.attention(_f64(q, dtype), _f64(k, dtype), _f64(v, dtype), s, causal)
+    mx, mn = _gpu.assert_close(_gpu.download(o, dtype), ref, dtype, f"d256 L{L}")
+    print(f"  d256 L{L}: max_abs {mx:.3e} mean_abs {mn:.3e}", flush=True)
 
 
 @pytest.mark.parametrize("causal", [False, True])
