@@ -169,6 +169,7 @@ def main():
     ap.add_argument("--no-unfused", action="store_true", help="skip the unfused baseline")
     ap.add_argument("--no-sweep", action="store_true", help="skip the sequence-length sweep (Table 3)")
     ap.add_argument("--no-d256", action="store_true", help="skip the head-dimension-256 workloads")
+    ap.add_argument("--no-softmax", action="store_true", help="skip the row-softmax operator")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="finish with two plain 256 MiB device copies (reference for byte counters)")
     args = ap.parse_args()
@@ -284,6 +285,26 @@ def main():
             del t3, o3
             torch.cuda.empty_cache()
 
+    smx = None
+    if not args.no_softmax:
+        # The row-softmax operator of Section 4.3: the paper's 512 x 512 and the
+        # score matrix of one L=16384 head; HBM-bound, so reported against 8 TB/s.
+        smx = []
+        hwq = capi.attn_hw_desc_query(torch.cuda.current_device())
+        for rows, n_cols in ((512, 512), (16384, 16384)):
+            print(f"bench: softmax {rows}x{n_cols}", file=sys.stderr, flush=True)
+            xs = upload(inputs.make_matrix(rows, n_cols, "bf16", seed=1301, spread=2.0), "bf16")
+            ys = torch.empty_like(xs)
+            rep = capi.attn_softmax_derive(hwq, rows, n_cols)
+            _, s_ms = time_steps(lambda: capi.attn_softmax(xs, ys), 50, 50)
+            smx.append({"rows": rows, "n": n_cols, "us": round(1e3 * s_ms, 2), "hbm_bytes": rep.hbm_bytes,
+                        "tbps": round(rep.hbm_bytes / (s_ms * 1e-3) / 1e12, 3),
+                        "frac_hbm": round(rep.hbm_bytes / (s_ms * 1e-3) / 1e12 / HBM_TBPS, 3),
+                        "tiles": {"split": rep.split, "resident_tiles": rep.resident_tiles, "passes": rep.passes,
+                                  "grid": rep.grid, "binding": rep.binding.decode()}})
+            del xs, ys
+        torch.cuda.empty_cache()
+
     cpu = None
     if not args.no_cpu:
         print("bench: cpu oracle", file=sys.stderr, flush=True)
@@ -328,6 +349,7 @@ def main():
         "secondary": secondary,
         "l_sweep": sweep,
         "head_dim_256": d256,
+        "softmax": smx,
         "cpu_baseline": cpu,
     }
     if args.copy_calibration:

@@ -179,13 +179,54 @@ int attn_fwd_merge(const void* workspace, size_t workspace_bytes, void* O,
                    int B, int H, int L, int d, float scale, int causal, int dtype, void* stream);
 
 /* Unfused baseline (Section 5.4, Table 3): three kernels on `stream` --
- * S = scale Q K^T written to the workspace in `dtype`, a row softmax
- * overwriting S with P (masked entries 0), then O = P V.  The workspace
- * holds B*H*L*L elements; size it with attn_unfused_workspace_bytes. */
+ * S = scale Q K^T written to the workspace in `dtype`, the row softmax of
+ * attn_softmax overwriting S with P (masked entries 0), then O = P V.  The
+ * workspace holds B*H*L*L elements; size it with attn_unfused_workspace_bytes.
+ * L must be a multiple of 8 (ATTN_E_SHAPE otherwise). */
 int attn_fwd_unfused(const void* Q, const void* K, const void* V, void* O,
                      int B, int H, int L, int d, float scale, int causal, int dtype,
                      void* workspace, size_t workspace_bytes, void* stream);
 size_t attn_unfused_workspace_bytes(int B, int H, int L, int dtype);
+
+/* Row softmax, the standalone online softmax of Section 4.3, on the same
+ * CU-centric derivation.  A tile is one 16-byte load per lane of a wave
+ * (wavefront_size * 16 / elem_bytes elements); the register budget (at the
+ * kernel's 2 waves per SIMD, less its fixed registers) fixes how many tiles a
+ * wave keeps resident, rounded down to a power of two; the CU rule splits a
+ * row over up to the 4 waves of a workgroup (their running maximum and
+ * denominator merged with the associative operator) until the grid reaches
+ * the CU count.  A row segment that fits the resident tiles is read from HBM
+ * once, else twice. */
+typedef struct {
+  int32_t feasible;
+  int32_t tile_elems;       /* elements one wave moves per tile */
+  int32_t resident_tiles;   /* tiles a wave keeps in registers */
+  int32_t split;            /* waves sharing one row (1 = none) */
+  int32_t waves_per_wg;
+  int32_t rows_per_wg;
+  int64_t seg;              /* row elements per wave (a multiple of 8) */
+  int64_t grid;             /* workgroups launched */
+  int32_t passes;           /* HBM reads of each element: 1 or 2 */
+  int32_t vgpr_est, vgpr_budget;
+  double wg_per_cu;
+  int64_t hbm_bytes;        /* bytes read and written by one call */
+  char binding[16];         /* "CU" (grid below the CU count), "VGPR" (two passes) or "none" */
+} attn_softmax_report_t;
+
+/* The derivation for a rows x n softmax of elem_bytes-byte elements.
+ * Host-only integer math; ATTN_E_ARG for a bad descriptor, ATTN_E_SHAPE for
+ * rows or n < 1. */
+int attn_softmax_derive(const attn_hw_desc_t* hw, int64_t rows, int64_t n, int elem_bytes,
+                        attn_softmax_report_t* out);
+
+/* Y = softmax(X) along each row: y_ij = exp(x_ij - max_j x_ij) / sum_j exp(...),
+ * X and Y [rows][n] contiguous in `dtype` (bf16 or f16), computed in fp32 and
+ * rounded to nearest-even.  causal != 0 treats X as square n x n blocks stacked
+ * along the rows and gives column j > (i mod n) of row i weight 0 (the
+ * top-left mask of attention scores).  Y may equal X.  Pointers need 2-byte
+ * alignment; with n % 8 == 0 and 16-byte aligned X and Y every access is a
+ * 16-byte one.  rows >= 1, 1 <= n <= 2^31.  Asynchronous on `stream`. */
+int attn_softmax(const void* X, void* Y, int64_t rows, int64_t n, int causal, int dtype, void* stream);
 
 /* Matrix-core layout probe (Section 3.1: fragment ownership must be checked
  * on the hardware).  Runs one 16x16x32 product with atom 0 = bf16, 1 = f16:

@@ -164,3 +164,49 @@ def derive(hw, atom, op, st):
     if hw.lds_bytes_per_clk > 0 and hw.mfma_flops_per_clk_cu > 0:
         rep["lds_bw_ok"] = t_q * hw.lds_bytes_per_clk >= hw.mfma_flops_per_clk_cu
     return rep
+
+
+# ---------------------------------------------------------------- row softmax
+
+@dataclasses.dataclass(frozen=True)
+class SoftmaxStructure:
+    """Fixed properties of the row-softmax kernel family (Section 4.3 operator)."""
+    waves_per_wg: int = 4
+    waves_per_simd: int = 2
+    vgpr_fixed: int = 48
+    load_bytes: int = 16      # bytes one lane moves per tile
+
+
+def derive_softmax(hw: Hardware, rows: int, n: int, elem_bytes: int, st: SoftmaxStructure = SoftmaxStructure()):
+    """The CU-centric rules applied to a bandwidth-bound row softmax.
+
+    Tile: one load of st.load_bytes per lane of a wave.  Registers: the budget
+    at st.waves_per_simd holds (budget - fixed) / (load_bytes / 4) tiles per
+    lane, kept as a power of two.  CU count: a row is split over 2, 4, ...
+    waves of a workgroup (never more waves than the workgroup has, never more
+    than one per tile) while the grid has fewer workgroups than CUs; the
+    per-wave running statistics are merged with the Section 4.3 operator.
+    Returns a dict, or None when not even one tile fits the registers.
+    """
+    if rows < 1 or n < 1:
+        raise ValueError("empty softmax")
+    per_lane = st.load_bytes // elem_bytes
+    tile = hw.wavefront_size * per_lane
+    budget = hw.vgpr_per_thread // st.waves_per_simd
+    regs = st.load_bytes // 4
+    fit = (budget - st.vgpr_fixed) // regs
+    if fit < 1:
+        return None
+    resident = 1 << int(math.floor(math.log2(fit)))
+    W = st.waves_per_wg
+    split = 1
+    while -(-rows * split // W) < hw.num_cus and split < W and split * tile < n:
+        split *= 2
+    grid = -(-rows * split // W)
+    seg = -(-(-(-n // split)) // 8) * 8
+    passes = 1 if seg <= resident * tile else 2
+    reread = min(n, split * (seg - resident * tile)) if passes == 2 else 0
+    binding = "VGPR" if passes == 2 else ("CU" if grid < hw.num_cus else "none")
+    return dict(tile_elems=tile, resident_tiles=resident, split=split, waves_per_wg=W, rows_per_wg=W // split,
+                seg=seg, grid=grid, passes=passes, vgpr_est=resident * regs + st.vgpr_fixed, vgpr_budget=budget,
+                hbm_bytes=rows * (2 * n + reread) * elem_bytes, binding=binding)

@@ -32,6 +32,7 @@ EXPORTS = (
     "attn_vgpr_estimate", "attn_tile_derive", "attn_fwd_plan", "attn_fwd", "attn_fwd_workspace_bytes",
     "attn_fwd_partial", "attn_fwd_merge", "attn_fwd_unfused",
     "attn_unfused_workspace_bytes", "attn_mfma_probe", "attn_strerror",
+    "attn_softmax_derive", "attn_softmax",
 )
 
 c_int, c_int32, c_int64, c_float, c_double, c_char, c_size_t, c_void_p, c_char_p = (
@@ -76,6 +77,14 @@ class TileReport(_Struct):
                 ("low_occupancy", c_int32), ("lds_bw_ok", c_int32), ("binding", c_char * 16)]
 
 
+class SoftmaxReport(_Struct):
+    _fields_ = [("feasible", c_int32), ("tile_elems", c_int32), ("resident_tiles", c_int32),
+                ("split", c_int32), ("waves_per_wg", c_int32), ("rows_per_wg", c_int32),
+                ("seg", c_int64), ("grid", c_int64), ("passes", c_int32), ("vgpr_est", c_int32),
+                ("vgpr_budget", c_int32), ("wg_per_cu", c_double), ("hbm_bytes", c_int64),
+                ("binding", c_char * 16)]
+
+
 class AttnError(RuntimeError):
     def __init__(self, status, msg):
         super().__init__(f"{STATUS.get(status, status)}: {msg}")
@@ -113,6 +122,8 @@ def load():
                                      c_int, c_float, c_int, c_int, c_void_p, c_size_t, c_void_p]),
         "attn_unfused_workspace_bytes": (c_size_t, [c_int, c_int, c_int, c_int]),
         "attn_mfma_probe": (c_int, [c_int, c_void_p, c_void_p, c_void_p, c_void_p]),
+        "attn_softmax_derive": (c_int, [P(HwDesc), c_int64, c_int64, c_int, P(SoftmaxReport)]),
+        "attn_softmax": (c_int, [c_void_p, c_void_p, c_int64, c_int64, c_int, c_int, c_void_p]),
         "attn_strerror": (c_char_p, [c_int]),
     }
     for name, (res, args) in sig.items():
@@ -262,3 +273,19 @@ def attn_fwd_unfused(q, k, v, o, scale: float, causal: bool, workspace, stream=N
 def attn_mfma_probe(atom: int, a, b, c, stream=None):
     """a: [16, 32], b: [32, 16] (bf16 or f16 device tensors), c: [16, 16] float32 device tensor."""
     _check(load().attn_mfma_probe(atom, _dev_ptr(a), _dev_ptr(b), _dev_ptr(c), _stream_ptr(a, stream)))
+
+
+def attn_softmax_derive(hw: HwDesc, rows: int, n: int, elem_bytes: int = 2) -> SoftmaxReport:
+    r = SoftmaxReport()
+    _check(load().attn_softmax_derive(ctypes.byref(hw), rows, n, elem_bytes, ctypes.byref(r)))
+    return r
+
+
+def attn_softmax(x, y, causal: bool = False, stream=None):
+    """y = softmax(x) along the last dimension (x, y contiguous, same shape and dtype; y may be x)."""
+    if tuple(y.shape) != tuple(x.shape) or y.dtype != x.dtype:
+        raise AttnError(CODE["ATTN_E_SHAPE"], "x and y must share shape and dtype")
+    n = x.shape[-1]
+    rows = x.numel() // n if n else 0
+    _check(load().attn_softmax(_dev_ptr(x), _dev_ptr(y), rows, n, int(causal), dtype_code(x),
+                               _stream_ptr(x, stream)))

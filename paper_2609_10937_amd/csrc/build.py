@@ -27,6 +27,7 @@ SOURCES = [
     "combine.hip",
     "probe.hip",
     "unfused.hip",
+    "softmax.hip",
     "fwd_bf16_d64.hip",
     "fwd_bf16_d128.hip",
     "fwd_f16_d64.hip",

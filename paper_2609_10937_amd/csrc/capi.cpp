@@ -404,9 +404,45 @@ int attn_fwd_unfused(const void* Q, const void* K, const void* V, void* O, int B
   if (!aligned16(workspace)) return ATTN_E_ALIGN;
   if (workspace_bytes < attn_unfused_workspace_bytes(B, H, L, dtype)) return ATTN_E_WORKSPACE;
   if ((int64_t)B * H > 65535 || (int64_t)B * H * L > 0x7fffffffLL) return ATTN_E_SHAPE;
-  const hipError_t e = launch_unfused(Q, K, V, O, workspace, B * H, L, d, scale, causal != 0, dtype,
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return ATTN_E_HIP;
+  attn_hw_desc_t desc;
+  rc = device_desc(dev, &desc);
+  if (rc != ATTN_OK) return rc;
+  attn_softmax_report_t sm;
+  rc = derive_softmax(&desc, (int64_t)B * H * L, L, 2, &sm);
+  if (rc != ATTN_OK) return rc;
+  if (sm.resident_tiles != kSoftmaxTiles || sm.waves_per_wg != kSoftmaxWaves) return ATTN_E_NO_INSTANCE;
+  const hipError_t e = launch_unfused(Q, K, V, O, workspace, B * H, L, d, scale, causal != 0, dtype, sm,
                                       static_cast<hipStream_t>(stream));
   return e == hipSuccess ? ATTN_OK : ATTN_E_HIP;
+}
+
+int attn_softmax_derive(const attn_hw_desc_t* hw, int64_t rows, int64_t n, int elem_bytes,
+                        attn_softmax_report_t* out) {
+  return derive_softmax(hw, rows, n, elem_bytes, out);
+}
+
+int attn_softmax(const void* X, void* Y, int64_t rows, int64_t n, int causal, int dtype, void* stream) {
+  if (!X || !Y) return ATTN_E_NULLPTR;
+  if (dtype != ATTN_BF16 && dtype != ATTN_F16) return ATTN_E_DTYPE;
+  if (rows < 1 || n < 1 || n > (int64_t(1) << 31)) return ATTN_E_SHAPE;
+  if (((uintptr_t)X & 1u) || ((uintptr_t)Y & 1u)) return ATTN_E_ALIGN;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return ATTN_E_HIP;
+  attn_hw_desc_t desc;
+  int rc = device_desc(dev, &desc);
+  if (rc != ATTN_OK) return rc;
+  attn_softmax_report_t rep;
+  rc = derive_softmax(&desc, rows, n, 2, &rep);
+  if (rc != ATTN_OK) return rc;
+  if (rep.resident_tiles != kSoftmaxTiles || rep.waves_per_wg != kSoftmaxWaves) return ATTN_E_NO_INSTANCE;
+  if (rep.grid > 0x7fffffffLL) return ATTN_E_SHAPE;
+  SoftmaxParams p{X, Y, rows, n, rep.seg, rep.split, causal != 0};
+  const bool aligned = n % 8 == 0 && aligned16(X) && aligned16(Y);
+  return launch_softmax(p, dtype, aligned, (unsigned)rep.grid, static_cast<hipStream_t>(stream)) == hipSuccess
+             ? ATTN_OK
+             : ATTN_E_HIP;
 }
 
 int attn_mfma_probe(int atom, const void* A, const void* Bm, float* C, void* stream) {

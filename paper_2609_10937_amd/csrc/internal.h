@@ -15,7 +15,7 @@ struct FwdParams {
   const void* v;
   void* o;
   float* part_o;    // [n_split, BH, L, d] unnormalised partial outputs (n_split > 1)
-  float* part_ml;   // [n_split, BH, L, 2] running max (raw logit units) and sum
+  float* part_ml;   // [n_split, BH, L, 2] reference point (base 2) and sum
   int BH;
   int L;
   int n_qt;             // query tiles per head
@@ -41,11 +41,30 @@ const FwdInstance* fwd_instances(int* count);
 
 hipError_t launch_combine(const FwdParams& p, int d, int dtype, hipStream_t s);
 
+// sm: the row-softmax derivation for the (B*H*L) x L score matrix.
 hipError_t launch_unfused(const void* q, const void* k, const void* v, void* o, void* ws,
                           int BH, int L, int d, float scale, int causal, int dtype,
-                          hipStream_t s);
+                          const attn_softmax_report_t& sm, hipStream_t s);
 
 hipError_t launch_mfma_probe(int atom, const void* a, const void* b, float* c, hipStream_t s);
+
+// Row softmax (Section 4.3).  x, y: [rows, n] contiguous; a wave owns `seg`
+// elements of a row and `split` waves share a row.
+struct SoftmaxParams {
+  const void* x;
+  void* y;
+  int64_t rows;
+  int64_t n;
+  int64_t seg;
+  int split;
+  int causal;   // mask column j > (row mod n)
+};
+// Fixed structure of the softmax kernel: waves per workgroup, waves per SIMD
+// (the register budget), registers outside the resident tiles, and the
+// resident tiles of the compiled kernel.
+constexpr int kSoftmaxWaves = 4, kSoftmaxWavesPerSimd = 2, kSoftmaxVgprFixed = 48, kSoftmaxTiles = 32;
+hipError_t launch_softmax(const SoftmaxParams& p, int dtype, bool aligned, unsigned grid, hipStream_t s);
+int derive_softmax(const attn_hw_desc_t* hw, int64_t rows, int64_t n, int elem_bytes, attn_softmax_report_t* rep);
 
 int derive_tiles(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const attn_op_t* op,
                  attn_tile_report_t* rep);

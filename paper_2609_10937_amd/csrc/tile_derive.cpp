@@ -38,7 +38,8 @@ int64_t vgpr_estimate(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, co
   return q_operand + scores + out_acc + stats + staging + op->vgpr_fixed;
 }
 
-static void set_binding(attn_tile_report_t* r, const char* s) {
+template <typename Report>
+static void set_binding(Report* r, const char* s) {
   memset(r->binding, 0, sizeof(r->binding));
   strncpy(r->binding, s, sizeof(r->binding) - 1);
 }
@@ -145,6 +146,58 @@ int derive_tiles(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const a
   rep->low_occupancy = grid < hw->num_cus;
   if (hw->lds_bytes_per_clk > 0 && hw->mfma_flops_per_clk_cu > 0)
     rep->lds_bw_ok = t_q * hw->lds_bytes_per_clk >= hw->mfma_flops_per_clk_cu;
+  set_binding(rep, binding);
+  return ATTN_OK;
+}
+
+// The row softmax (Section 4.3) on the same CU-centric rules:
+//   tile      one 16-byte load per lane: wavefront_size * 16 / elem_bytes elements;
+//   registers the budget at the kernel's waves per SIMD, less its fixed
+//             registers, holds R = (budget - fixed) / (16 / 4) packed tiles per
+//             lane, rounded down to a power of two (the compiled instances);
+//   CU count  split a row over 2, 4, ... waves of the workgroup (at most all of
+//             them, at most one per tile) while the grid is below the CU count.
+int derive_softmax(const attn_hw_desc_t* hw, int64_t rows, int64_t n, int elem_bytes, attn_softmax_report_t* rep) {
+  if (!hw || !rep) return ATTN_E_NULLPTR;
+  if (hw->vgpr_per_thread <= 0 || hw->wavefront_size <= 0 || hw->num_cus <= 0 || elem_bytes <= 0 ||
+      16 % elem_bytes != 0)
+    return ATTN_E_ARG;
+  if (rows < 1 || n < 1) return ATTN_E_SHAPE;
+  memset(rep, 0, sizeof(*rep));
+  const int64_t W = kSoftmaxWaves;
+  const int64_t per_lane = 16 / elem_bytes;
+  const int64_t tile = (int64_t)hw->wavefront_size * per_lane;
+  const int64_t budget = hw->vgpr_per_thread / kSoftmaxWavesPerSimd;
+  const int64_t regs_per_tile = 16 / 4;
+  rep->vgpr_budget = (int32_t)budget;
+  if (budget < kSoftmaxVgprFixed + regs_per_tile) {
+    rep->feasible = 0;
+    set_binding(rep, "VGPR");
+    return ATTN_E_INFEASIBLE;
+  }
+  int64_t resident = 1;
+  while (2 * resident <= (budget - kSoftmaxVgprFixed) / regs_per_tile) resident *= 2;
+  int64_t split = 1;
+  const char* binding = "none";
+  while (cdiv(rows * split, W) < hw->num_cus && split < W && split * tile < n) split *= 2;
+  const int64_t grid = cdiv(rows * split, W);
+  if (grid < hw->num_cus) binding = "CU";
+  const int64_t seg = cdiv(cdiv(n, split), 8) * 8;
+  const int passes = seg <= resident * tile ? 1 : 2;
+  if (passes == 2) binding = "VGPR";
+  const int64_t reread = passes == 2 ? std::min<int64_t>(n, split * (seg - resident * tile)) : 0;
+  rep->feasible = 1;
+  rep->tile_elems = (int32_t)tile;
+  rep->resident_tiles = (int32_t)resident;
+  rep->split = (int32_t)split;
+  rep->waves_per_wg = (int32_t)W;
+  rep->rows_per_wg = (int32_t)(W / split);
+  rep->seg = seg;
+  rep->grid = grid;
+  rep->passes = passes;
+  rep->vgpr_est = (int32_t)(resident * regs_per_tile + kSoftmaxVgprFixed);
+  rep->wg_per_cu = (double)grid / hw->num_cus;
+  rep->hbm_bytes = rows * (2 * n + reread) * elem_bytes;
   set_binding(rep, binding);
   return ATTN_OK;
 }

@@ -1,7 +1,8 @@
 // Unfused attention baseline (Section 5.4, Table 3): the L x L score matrix
 // goes to device memory between three kernels.
 //   gemm (A B^T):  S = scale Q K^T, stored in the input type
-//   softmax_rows:  S -> P in place, causal-masked entries 0
+//   softmax:       S -> P in place, causal-masked entries 0 (the row-softmax
+//                  operator of Section 4.3, attn_softmax, on its own tiles)
 //   gemm (A B):    O = P V
 // The products use the same 16x16x32 matrix-core atom and fragment layouts as
 // the fused kernel; operands are staged through LDS in 16-byte chunks.
@@ -156,52 +157,9 @@ __global__ void __launch_bounds__(256) gemm_kernel(const uint16_t* __restrict__ 
       }
 }
 
-// Row softmax in place over rows of length L (row index = head * L + i).
-// Pass 1 keeps a running (max, sum) per thread and merges them across the
-// workgroup; pass 2 rewrites the row as probabilities (0 where masked).
-template <int DT>
-__global__ void __launch_bounds__(256) softmax_rows_kernel(uint16_t* __restrict__ Sm, int L, int causal) {
-  using S = typename Mfma<DT>::S;
-  constexpr float LOG2E = 1.4426950408889634f;
-  const int64_t row = blockIdx.x;
-  const int i = (int)(row % L);
-  const int n = causal ? i + 1 : L;
-  uint16_t* sr = Sm + row * (int64_t)L;
-  auto ld = [&](int j) { return (float)__builtin_bit_cast(S, sr[j]); };
-
-  float m = -INFINITY, s = 0.f;
-  for (int j = threadIdx.x; j < n; j += 256) {
-    const float x = ld(j);
-    const float mn = fmaxf(m, x);
-    s = s * exp2_hw((m - mn) * LOG2E) + exp2_hw((x - mn) * LOG2E);
-    m = mn;
-  }
-  __shared__ float red_m[256], red_s[256];
-  red_m[threadIdx.x] = m;
-  red_s[threadIdx.x] = s;
-  __syncthreads();
-  for (int off = 128; off > 0; off >>= 1) {
-    if (threadIdx.x < off) {
-      const float ma = red_m[threadIdx.x], mb = red_m[threadIdx.x + off];
-      const float mn = fmaxf(ma, mb);
-      const float wa = ma == -INFINITY ? 0.f : exp2_hw((ma - mn) * LOG2E);
-      const float wb = mb == -INFINITY ? 0.f : exp2_hw((mb - mn) * LOG2E);
-      red_s[threadIdx.x] = red_s[threadIdx.x] * wa + red_s[threadIdx.x + off] * wb;
-      red_m[threadIdx.x] = mn;
-    }
-    __syncthreads();
-  }
-  const float mx = red_m[0];
-  const float inv = 1.f / red_s[0];
-  for (int j = threadIdx.x; j < L; j += 256) {
-    const float pv = j < n ? exp2_hw((ld(j) - mx) * LOG2E) * inv : 0.f;
-    sr[j] = __builtin_bit_cast(uint16_t, (S)pv);
-  }
-}
-
 template <int DT>
 static hipError_t run_unfused(const void* q, const void* k, const void* v, void* o, void* ws, int BH, int L,
-                              int d, float scale, int causal, hipStream_t s) {
+                              int d, float scale, int causal, const attn_softmax_report_t& sm, hipStream_t s) {
   const uint16_t* Q = static_cast<const uint16_t*>(q);
   const uint16_t* K = static_cast<const uint16_t*>(k);
   const uint16_t* V = static_cast<const uint16_t*>(v);
@@ -211,8 +169,8 @@ static hipError_t run_unfused(const void* q, const void* k, const void* v, void*
                      Q, K, Sm, L, L, d, scale);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((softmax_rows_kernel<DT>), dim3((unsigned)((int64_t)BH * L)), dim3(256), 0, s, Sm, L, causal);
-  e = hipGetLastError();
+  const SoftmaxParams sp{Sm, Sm, (int64_t)BH * L, L, sm.seg, sm.split, causal};
+  e = launch_softmax(sp, DT, true, (unsigned)sm.grid, s);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((gemm_kernel<DT, true, 64>), dim3((L + 63) / 64, (d + 127) / 128, BH), dim3(256), 0, s,
                      static_cast<const uint16_t*>(Sm), V, O, L, d, L, 1.0f);
@@ -220,9 +178,9 @@ static hipError_t run_unfused(const void* q, const void* k, const void* v, void*
 }
 
 hipError_t launch_unfused(const void* q, const void* k, const void* v, void* o, void* ws, int BH, int L, int d,
-                          float scale, int causal, int dtype, hipStream_t s) {
-  if (dtype == ATTN_BF16) return run_unfused<ATTN_BF16>(q, k, v, o, ws, BH, L, d, scale, causal, s);
-  return run_unfused<ATTN_F16>(q, k, v, o, ws, BH, L, d, scale, causal, s);
+                          float scale, int causal, int dtype, const attn_softmax_report_t& sm, hipStream_t s) {
+  if (dtype == ATTN_BF16) return run_unfused<ATTN_BF16>(q, k, v, o, ws, BH, L, d, scale, causal, sm, s);
+  return run_unfused<ATTN_F16>(q, k, v, o, ws, BH, L, d, scale, causal, sm, s);
 }
 
 }  // namespace attn

@@ -136,5 +136,16 @@ def make_qkv(B: int, H: int, L: int, d: int, dtype: str, seed: int, k_scale: flo
     return out[0], out[1], out[2]
 
 
+def make_matrix(rows: int, n: int, dtype: str, seed: int, spread: float = 1.0):
+    """A rows x n matrix of N(0,1) float32 values times `spread` (in float32),
+    rounded once to the storage type; returns the uint16 bit patterns."""
+    if dtype not in DTYPES:
+        raise ValueError(f"unknown dtype {dtype!r}")
+    x = np.random.Generator(np.random.PCG64(seed)).standard_normal((rows, n), dtype=np.float32)
+    if spread != 1.0:
+        x *= np.float32(spread)
+    return round_bits(x, dtype)
+
+
 def workload_inputs(w: Workload):
     return make_qkv(w.B, w.H, w.L, w.d, w.dtype, w.seed, w.k_scale)
