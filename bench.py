@@ -170,6 +170,7 @@ def main():
     ap.add_argument("--no-sweep", action="store_true", help="skip the sequence-length sweep (Table 3)")
     ap.add_argument("--no-d256", action="store_true", help="skip the head-dimension-256 workloads")
     ap.add_argument("--no-softmax", action="store_true", help="skip the row-softmax operator")
+    ap.add_argument("--no-gemm", action="store_true", help="skip the GEMM operator")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="finish with two plain 256 MiB device copies (reference for byte counters)")
     args = ap.parse_args()
@@ -305,6 +306,32 @@ def main():
             del xs, ys
         torch.cuda.empty_cache()
 
+    gemm = None
+    if not args.no_gemm:
+        # The GEMM of Section 4 (Figure 1's 4096^3, bf16 inputs, fp32 accumulate and
+        # output) on the derived tiles; torch.mm (the vendor library, bf16 output)
+        # on the same inputs for reference.
+        M = N = K = 4096
+        print(f"bench: gemm {M}x{N}x{K}", file=sys.stderr, flush=True)
+        hwq = capi.attn_hw_desc_query(torch.cuda.current_device())
+        rep = capi.attn_gemm_derive(hwq, capi.attn_atom_preset("bf16_16x16x32"), M, N, K)
+        ga = upload(inputs.make_matrix(M, K, "bf16", seed=1401), "bf16")
+        gb = upload(inputs.make_matrix(K, N, "bf16", seed=1402), "bf16")
+        gc = torch.empty((M, N), dtype=torch.float32, device="cuda")
+        _, g_ms = time_steps(lambda: capi.attn_gemm(ga, gb, gc), 50, 50)
+        _, t_ms = time_steps(lambda: torch.mm(ga, gb), 50, 50)
+        gfl = 2.0 * M * N * K
+        gemm = {"M": M, "N": N, "K": K, "dtype": "bf16", "out": "f32", "us": round(1e3 * g_ms, 2),
+                "tflops": round(gfl / (g_ms * 1e-3) / 1e12, 1),
+                "frac_peak": round(gfl / (g_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                "torch_mm_bf16_us": round(1e3 * t_ms, 2),
+                "torch_mm_tflops": round(gfl / (t_ms * 1e-3) / 1e12, 1),
+                "tiles": {"t_m": rep.t_m, "t_n": rep.t_n, "t_k": rep.t_k, "warp_m": rep.warp_m,
+                          "warp_n": rep.warp_n, "grid": rep.grid, "vgpr_est": rep.vgpr_est,
+                          "binding": rep.binding.decode()}}
+        del ga, gb, gc
+        torch.cuda.empty_cache()
+
     cpu = None
     if not args.no_cpu:
         print("bench: cpu oracle", file=sys.stderr, flush=True)
@@ -350,6 +377,7 @@ def main():
         "l_sweep": sweep,
         "head_dim_256": d256,
         "softmax": smx,
+        "gemm": gemm,
         "cpu_baseline": cpu,
     }
     if args.copy_calibration:

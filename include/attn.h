@@ -228,6 +228,50 @@ int attn_softmax_derive(const attn_hw_desc_t* hw, int64_t rows, int64_t n, int e
  * 16-byte one.  rows >= 1, 1 <= n <= 2^31.  Asynchronous on `stream`. */
 int attn_softmax(const void* X, void* Y, int64_t rows, int64_t n, int causal, int dtype, void* stream);
 
+/* GEMM C = A B (Section 4's worked example, Figure 1): workgroup tile
+ * t_M x t_N x t_K and per-wave tile from the same closed-form rules as the
+ * attention tiles, for the GEMM kernel's fixed structure (5 LDS stages of an
+ * A and a B tile, 2 x 4 waves, 2 waves per SIMD):
+ *   LDS      t_M = t_N = floor(sqrt(LDS / elem)), aligned down to the atom
+ *            times the waves along each side; t_K = floor(LDS / (stages
+ *            (t_M + t_N) elem)), aligned down to the atom's k and to whole
+ *            1 KB copy blocks per wave;
+ *   VGPR     the per-wave accumulators, (t_M / 2)(t_N / 4) fp32 values over
+ *            the wavefront, plus the fixed registers within the budget at
+ *            2 waves per SIMD (the larger side halves until they fit);
+ *   CU count while ceil(M / t_M) ceil(N / t_N) is below the CU count the
+ *            larger side halves, down to one atom per wave.
+ * Section 4 prints the LDS rule with LDS / 2 under the square root; the
+ * section's own numbers (128 x 128 x 32 for 64 KB, 4-byte elements, two
+ * stages) follow from LDS / elem, which is the reading taken here. */
+typedef struct {
+  int32_t feasible;
+  int32_t t_m, t_n, t_k;        /* workgroup (CU) tile */
+  int32_t warp_m, warp_n;       /* per-wave tile of C */
+  int32_t stages, waves_per_wg;
+  int64_t grid;                 /* workgroups: ceil(M / t_m) ceil(N / t_n) */
+  int32_t vgpr_est, vgpr_budget;
+  int64_t lds_used, lds_budget;
+  double wg_per_cu;
+  char binding[16];             /* "LDS", "VGPR" or "CU" */
+} attn_gemm_report_t;
+
+/* The derivation for an M x N x K product with `atom` (its in_bytes is the
+ * element size).  Host-only integer math; ATTN_E_ARG for a bad descriptor or
+ * atom, ATTN_E_SHAPE for M, N or K < 1, ATTN_E_INFEASIBLE when not even one
+ * atom per wave fits (report.binding says which resource). */
+int attn_gemm_derive(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, int64_t M, int64_t N, int64_t K,
+                     attn_gemm_report_t* out);
+
+/* C = A B on the matrix cores: A [M][K] and B [K][N] row-major in `dtype`
+ * (bf16 or f16), C [M][N] row-major fp32, every product and sum in fp32
+ * (Section 4: the GEMM validated against a double-precision reference).
+ * Tiles come from attn_gemm_derive on the current device's descriptor.
+ * Sizes: 1 <= M < 2^31; 8 <= N <= 2^24 and 8 <= K <= 2^22, both multiples of
+ * 8 (ATTN_E_SHAPE otherwise); A, B and C 16-byte aligned (ATTN_E_ALIGN).  C
+ * must not overlap A or B.  Asynchronous on `stream`. */
+int attn_gemm(const void* A, const void* B, float* C, int64_t M, int64_t N, int64_t K, int dtype, void* stream);
+
 /* Matrix-core layout probe (Section 3.1: fragment ownership must be checked
  * on the hardware).  Runs one 16x16x32 product with atom 0 = bf16, 1 = f16:
  * A is a row-major 16 x 32 device array, Bm a row-major 32 x 16 array, C a

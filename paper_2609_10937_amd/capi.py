@@ -32,7 +32,7 @@ EXPORTS = (
     "attn_vgpr_estimate", "attn_tile_derive", "attn_fwd_plan", "attn_fwd", "attn_fwd_workspace_bytes",
     "attn_fwd_partial", "attn_fwd_merge", "attn_fwd_unfused",
     "attn_unfused_workspace_bytes", "attn_mfma_probe", "attn_strerror",
-    "attn_softmax_derive", "attn_softmax",
+    "attn_softmax_derive", "attn_softmax", "attn_gemm_derive", "attn_gemm",
 )
 
 c_int, c_int32, c_int64, c_float, c_double, c_char, c_size_t, c_void_p, c_char_p = (
@@ -85,6 +85,13 @@ class SoftmaxReport(_Struct):
                 ("binding", c_char * 16)]
 
 
+class GemmReport(_Struct):
+    _fields_ = [("feasible", c_int32), ("t_m", c_int32), ("t_n", c_int32), ("t_k", c_int32),
+                ("warp_m", c_int32), ("warp_n", c_int32), ("stages", c_int32), ("waves_per_wg", c_int32),
+                ("grid", c_int64), ("vgpr_est", c_int32), ("vgpr_budget", c_int32), ("lds_used", c_int64),
+                ("lds_budget", c_int64), ("wg_per_cu", c_double), ("binding", c_char * 16)]
+
+
 class AttnError(RuntimeError):
     def __init__(self, status, msg):
         super().__init__(f"{STATUS.get(status, status)}: {msg}")
@@ -124,6 +131,8 @@ def load():
         "attn_mfma_probe": (c_int, [c_int, c_void_p, c_void_p, c_void_p, c_void_p]),
         "attn_softmax_derive": (c_int, [P(HwDesc), c_int64, c_int64, c_int, P(SoftmaxReport)]),
         "attn_softmax": (c_int, [c_void_p, c_void_p, c_int64, c_int64, c_int, c_int, c_void_p]),
+        "attn_gemm_derive": (c_int, [P(HwDesc), P(Atom), c_int64, c_int64, c_int64, P(GemmReport)]),
+        "attn_gemm": (c_int, [c_void_p, c_void_p, c_void_p, c_int64, c_int64, c_int64, c_int, c_void_p]),
         "attn_strerror": (c_char_p, [c_int]),
     }
     for name, (res, args) in sig.items():
@@ -289,3 +298,26 @@ def attn_softmax(x, y, causal: bool = False, stream=None):
     rows = x.numel() // n if n else 0
     _check(load().attn_softmax(_dev_ptr(x), _dev_ptr(y), rows, n, int(causal), dtype_code(x),
                                _stream_ptr(x, stream)))
+
+
+def attn_gemm_derive(hw: HwDesc, atom: Atom, M: int, N: int, K: int) -> GemmReport:
+    r = GemmReport()
+    _check(load().attn_gemm_derive(ctypes.byref(hw), ctypes.byref(atom), M, N, K, ctypes.byref(r)))
+    return r
+
+
+def attn_gemm(a, b, c, stream=None):
+    """c = a @ b: a [M, K] and b [K, N] contiguous bf16 or f16 device tensors of one
+    dtype, c [M, N] contiguous float32."""
+    if a.dim() != 2 or b.dim() != 2 or c.dim() != 2:
+        raise AttnError(CODE["ATTN_E_SHAPE"], "a, b and c must be matrices")
+    M, K = a.shape
+    if b.shape[0] != K or tuple(c.shape) != (M, b.shape[1]):
+        raise AttnError(CODE["ATTN_E_SHAPE"], f"shapes {tuple(a.shape)} @ {tuple(b.shape)} -> {tuple(c.shape)}")
+    if b.dtype != a.dtype:
+        raise AttnError(CODE["ATTN_E_DTYPE"], "a and b must share a dtype")
+    import torch
+    if c.dtype != torch.float32:
+        raise AttnError(CODE["ATTN_E_DTYPE"], "c must be float32")
+    _check(load().attn_gemm(_dev_ptr(a), _dev_ptr(b), _dev_ptr(c), M, b.shape[1], K, dtype_code(a),
+                            _stream_ptr(a, stream)))

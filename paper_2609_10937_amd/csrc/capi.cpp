@@ -8,6 +8,7 @@
 #include <tuple>
 #include <vector>
 
+#include "gemm_internal.h"
 #include "internal.h"
 
 namespace attn {
@@ -443,6 +444,41 @@ int attn_softmax(const void* X, void* Y, int64_t rows, int64_t n, int causal, in
   return launch_softmax(p, dtype, aligned, (unsigned)rep.grid, static_cast<hipStream_t>(stream)) == hipSuccess
              ? ATTN_OK
              : ATTN_E_HIP;
+}
+
+int attn_gemm_derive(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, int64_t M, int64_t N, int64_t K,
+                     attn_gemm_report_t* out) {
+  return derive_gemm(hw, atom, M, N, K, out);
+}
+
+int attn_gemm(const void* A, const void* B, float* C, int64_t M, int64_t N, int64_t K, int dtype, void* stream) {
+  if (!A || !B || !C) return ATTN_E_NULLPTR;
+  if (dtype != ATTN_BF16 && dtype != ATTN_F16) return ATTN_E_DTYPE;
+  // 32-bit lane offsets within a workgroup's panels: t_M K 2 and t_K N 2
+  // bytes stay below 2^32 for K <= 2^22 and N <= 2^24.
+  if (M < 1 || M > 0x7fffffffLL || N < 8 || N > (int64_t(1) << 24) || N % 8 != 0 || K < 8 ||
+      K > (int64_t(1) << 22) || K % 8 != 0)
+    return ATTN_E_SHAPE;
+  if (!aligned16(A) || !aligned16(B) || !aligned16(C)) return ATTN_E_ALIGN;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return ATTN_E_HIP;
+  attn_hw_desc_t desc;
+  int rc = device_desc(dev, &desc);
+  if (rc != ATTN_OK) return rc;
+  const attn_mfma_atom_t atom = {16, 16, 32, 2, 4};
+  attn_gemm_report_t rep;
+  rc = derive_gemm(&desc, &atom, M, N, K, &rep);
+  if (rc != ATTN_OK) return rc;
+  const int64_t n_tm = (M + rep.t_m - 1) / rep.t_m, n_tn = (N + rep.t_n - 1) / rep.t_n;
+  if (n_tm * n_tn > 0x7fffffffLL) return ATTN_E_SHAPE;
+  const GemmInstance* inst = nullptr;
+  int n = 0;
+  const GemmInstance* table = dtype == ATTN_BF16 ? gemm_instances_bf16(&n) : gemm_instances_f16(&n);
+  for (int i = 0; i < n; ++i)
+    if (table[i].t_m == rep.t_m && table[i].t_n == rep.t_n && table[i].t_k == rep.t_k) inst = &table[i];
+  if (!inst) return ATTN_E_NO_INSTANCE;
+  const GemmParams p{A, B, C, (int)M, (int)N, (int)K, (int)n_tm, (int)n_tn};
+  return inst->launch(p, static_cast<hipStream_t>(stream)) == hipSuccess ? ATTN_OK : ATTN_E_HIP;
 }
 
 int attn_mfma_probe(int atom, const void* A, const void* Bm, float* C, void* stream) {

@@ -19,8 +19,10 @@
 #include <string.h>
 
 #include <algorithm>
+#include <cmath>
 #include <numeric>
 
+#include "gemm_internal.h"
 #include "internal.h"
 
 namespace attn {
@@ -198,6 +200,97 @@ int derive_softmax(const attn_hw_desc_t* hw, int64_t rows, int64_t n, int elem_b
   rep->vgpr_est = (int32_t)(resident * regs_per_tile + kSoftmaxVgprFixed);
   rep->wg_per_cu = (double)grid / hw->num_cus;
   rep->hbm_bytes = rows * (2 * n + reread) * elem_bytes;
+  set_binding(rep, binding);
+  return ATTN_OK;
+}
+
+// The GEMM of Section 4 (its worked example) on the same rules, for the GEMM
+// kernel's fixed structure (gemm_internal.h):
+//   LDS       square tile t = floor(sqrt(LDS / elem)) (the reading of the
+//             printed formula that reproduces the section's own numbers),
+//             each side aligned down to the atom times the waves along it;
+//             t_K = floor(LDS / (stages (t_M + t_N) elem)), aligned down to
+//             the atom's k and to whole copy blocks of both tiles per wave;
+//   VGPR      per wave (t_M / W_M)(t_N / W_N) fp32 accumulators plus the
+//             fixed registers within the budget at the kernel's waves per
+//             SIMD: the larger side halves until they fit;
+//   CU count  while the grid is below the CU count the larger side halves,
+//             down to one atom per wave.
+static int64_t gemm_vgpr(const attn_mfma_atom_t* atom, int64_t wave_words, int64_t tm, int64_t tn) {
+  const int64_t wm = tm / kGemmWavesM, wn = tn / kGemmWavesN;
+  const int64_t per_atom = cdiv((int64_t)atom->m * atom->n * atom->acc_bytes, wave_words);
+  return (wm / atom->m) * (wn / atom->n) * per_atom + kGemmVgprFixed;
+}
+
+static int64_t gemm_t_k(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, int64_t tm, int64_t tn) {
+  const int64_t elem = atom->in_bytes;
+  const int64_t unit = (int64_t)kGemmCopyBlock * kGemmWavesM * kGemmWavesN;
+  int64_t step = atom->k;
+  for (const int64_t side : {tm, tn}) {
+    const int64_t need = unit / std::gcd(unit, side * elem);
+    step = std::lcm(step, need);
+  }
+  return hw->lds_bytes / (kGemmStages * (tm + tn) * elem) / step * step;
+}
+
+int derive_gemm(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, int64_t M, int64_t N, int64_t K,
+                attn_gemm_report_t* rep) {
+  if (!hw || !atom || !rep) return ATTN_E_NULLPTR;
+  if (hw->lds_bytes <= 0 || hw->vgpr_per_thread <= 0 || hw->wavefront_size <= 0 || hw->num_cus <= 0)
+    return ATTN_E_ARG;
+  if (atom->m <= 0 || atom->n <= 0 || atom->k <= 0 || atom->in_bytes <= 0 || atom->acc_bytes <= 0)
+    return ATTN_E_ARG;
+  if (M < 1 || N < 1 || K < 1) return ATTN_E_SHAPE;
+  memset(rep, 0, sizeof(*rep));
+  rep->stages = kGemmStages;
+  rep->waves_per_wg = kGemmWavesM * kGemmWavesN;
+  rep->lds_budget = hw->lds_bytes;
+  const int64_t budget = hw->vgpr_per_thread / kGemmWavesPerSimd;
+  rep->vgpr_budget = (int32_t)budget;
+  const int64_t am = (int64_t)atom->m * kGemmWavesM, an = (int64_t)atom->n * kGemmWavesN;
+  const int64_t wave_words = 4 * (int64_t)hw->wavefront_size;
+  const int64_t q = hw->lds_bytes / atom->in_bytes;
+  int64_t t = (int64_t)std::sqrt((double)q);  // floor(sqrt(q)), corrected to be exact
+  while (t * t > q) --t;
+  while ((t + 1) * (t + 1) <= q) ++t;
+  int64_t tm = t / am * am, tn = t / an * an;
+  const char* binding = "LDS";
+  if (tm < am || tn < an) {
+    set_binding(rep, "LDS");
+    return ATTN_E_INFEASIBLE;
+  }
+  while (gemm_vgpr(atom, wave_words, tm, tn) > budget) {
+    if (tm >= tn && tm > am) {
+      tm = std::max(am, tm / 2 / am * am);
+    } else if (tn > an) {
+      tn = std::max(an, tn / 2 / an * an);
+    } else {
+      set_binding(rep, "VGPR");
+      return ATTN_E_INFEASIBLE;
+    }
+    binding = "VGPR";
+  }
+  while (cdiv(M, tm) * cdiv(N, tn) < hw->num_cus && (tm > am || tn > an)) {
+    if ((tm >= tn && tm > am) || tn <= an) tm = std::max(am, tm / 2 / am * am);
+    else tn = std::max(an, tn / 2 / an * an);
+    binding = "CU";
+  }
+  const int64_t tk = gemm_t_k(hw, atom, tm, tn);
+  if (tk < atom->k) {
+    set_binding(rep, "LDS");
+    return ATTN_E_INFEASIBLE;
+  }
+  const int64_t grid = cdiv(M, tm) * cdiv(N, tn);
+  rep->feasible = 1;
+  rep->t_m = (int32_t)tm;
+  rep->t_n = (int32_t)tn;
+  rep->t_k = (int32_t)tk;
+  rep->warp_m = (int32_t)(tm / kGemmWavesM);
+  rep->warp_n = (int32_t)(tn / kGemmWavesN);
+  rep->grid = grid;
+  rep->vgpr_est = (int32_t)gemm_vgpr(atom, wave_words, tm, tn);
+  rep->lds_used = (int64_t)kGemmStages * (tm + tn) * tk * atom->in_bytes;
+  rep->wg_per_cu = (double)grid / hw->num_cus;
   set_binding(rep, binding);
   return ATTN_OK;
 }
