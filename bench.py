@@ -144,6 +144,31 @@ def measured_mfma(workload):
             "source": "profiles/fwd_kernel_mfma_busy.md"}
 
 
+def gemm_source_hash():
+    """Hash of the GEMM kernel's sources (counter figures taken on other sources are stale)."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_10937_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.startswith("gemm_"):
+            with open(os.path.join(csrc, name), "rb") as f:
+                h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_gemm_counters():
+    """HBM bytes and matrix-core busy fraction of the 4096^3 GEMM from the committed
+    counter summary, if it was taken on the current GEMM sources (else None)."""
+    try:
+        with open(os.path.join(ROOT, "profiles", "gemm_4096_bf16_counters.json")) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("gemm_source_hash") != gemm_source_hash():
+        return None
+    return rec["kernels"]["attn_gemm"]
+
+
 def sampled_parity(w, q, k, v, out):
     from oracle import attention as A
     import torch
@@ -321,9 +346,17 @@ def main():
         _, g_ms = time_steps(lambda: capi.attn_gemm(ga, gb, gc), 50, 50)
         _, t_ms = time_steps(lambda: torch.mm(ga, gb), 50, 50)
         gfl = 2.0 * M * N * K
+        gc_ = measured_gemm_counters()
         gemm = {"M": M, "N": N, "K": K, "dtype": "bf16", "out": "f32", "us": round(1e3 * g_ms, 2),
                 "tflops": round(gfl / (g_ms * 1e-3) / 1e12, 1),
                 "frac_peak": round(gfl / (g_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                "roofline": {"bound": "mfma", "achieved": round(gfl / (g_ms * 1e-3) / 1e12, 1),
+                             "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                             "frac": round(gfl / (g_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                             "traffic": None if gc_ is None else gc_["hbm_bytes_per_launch"],
+                             "algorithmic_bytes": 2 * M * K * 2 + M * N * 4,
+                             "mfma_busy_frac": None if gc_ is None else gc_["mfma_busy_frac"],
+                             "clock_ghz": None if gc_ is None else gc_["clock_ghz"]},
                 "torch_mm_bf16_us": round(1e3 * t_ms, 2),
                 "torch_mm_tflops": round(gfl / (t_ms * 1e-3) / 1e12, 1),
                 "tiles": {"t_m": rep.t_m, "t_n": rep.t_n, "t_k": rep.t_k, "warp_m": rep.warp_m,

@@ -12,17 +12,25 @@
 //   B-role (A^T): lane holds A[c][8g + e]
 //   result:       lane holds C[c][4g + r], r = 0..3
 // so the k index of both operands is 8g + e: a lane's A^T fragment is one
-// 16-byte chunk of a row of the A tile (ds_read_b128) and its B^T fragment
+// 16-byte chunk of a row of A (ds_read_b128) and its B^T fragment
 // four rows of one column of the B tile, read twice with the transposing
 // ds_read_b64_tr_b16 (lane j of a 16-lane group addresses row k0 + j/4,
 // columns n0 + 4(j%4) .. +3; lane i receives rows k0 .. k0+3 of column n0+i).
 //
-// LDS holds ST stages, each an A tile [t_M][t_K] and a B tile [t_K][t_N],
-// row-major in 16-byte chunks, chunk positions XOR-swizzled per row so that
-// the reads of a 16-lane group (b128) or of a 32-lane half (tr_b64) touch
-// distinct banks (64 banks of 4 bytes: 16 chunk positions per bank row).
-// Tiles move HBM -> LDS with global_load_lds_dwordx4 (each wave copies whole
-// 1 KB blocks of both tiles), so no registers stage them.
+// LDS holds ST stages, each an A tile and a B tile (64 banks of 4 bytes:
+// 16 chunk positions of 16 bytes per 256-byte bank row).  A b128 read is
+// served 16 lanes at a time, and the bank-conflict counter rules out every
+// grouping except lanes sharing lane-index bits {0, 5} or {1, 4}; the
+// layouts below keep each such group on 16 distinct positions.
+//  A tile, t_K = 32 (64-byte rows, four to a bank row, so no row-major
+//    swizzle can spread a group): 1 KB blocks of 16 rows x 32 k, one per
+//    atom fragment, slot 16 q + p holding row p ^ q, 16-byte k chunk q.
+//  A tile, t_K >= 64: row-major [t_M][t_K], chunk positions XOR-swizzled
+//    per row (whole rows per copy keep the global reads line-sized).
+//  B tile: row-major [t_K][t_N], chunk positions XOR-swizzled per row for
+//    the transposing reads.
+// Tiles move HBM -> LDS with global_load_lds_dwordx4 (each wave copies
+// whole 1 KB blocks of both tiles), so no registers stage them.
 //
 // Pipeline.  Eight waves (2 along M x 4 along N, two per SIMD) take one
 // step per k tile: the step's matrix products, with this wave's copies of the
@@ -38,25 +46,22 @@
 
 namespace attn {
 
-// Chunk swizzle of the A tile: rows of KCA chunks (16 / KCA rows per 256-byte
-// bank row); the 16 rows that a b128 read of a 16-lane group touches (one
-// logical chunk each) land on 16 distinct chunk positions.
+// Chunk swizzle of a row-major A tile with KCA >= 8 chunks per row.
 template <int KCA>
 __device__ __forceinline__ int gemm_a_swz(int r) {
-  static_assert(KCA == 4 || KCA == 8 || KCA == 16, "A row chunks");
+  static_assert(KCA == 8 || KCA == 16, "A row chunks");
   if constexpr (KCA == 16) return r & 15;
-  else if constexpr (KCA == 8) return (r >> 1) & 7;
-  else return (r >> 2) & 3;
+  else return (r >> 1) & 7;
 }
-// Chunk swizzle of the B tile: rows of KCB chunks.  A 32-lane half of a
-// transposing read covers rows {0..3, 8..11} (+4, +16, +32 kk) at one
-// logical pair of chunks; even swizzle values keep the pair adjacent and
-// give the eight rows distinct pair positions.
+// Chunk swizzle of the B tile: rows of KCB chunks.  A transposing read is
+// served 16 lanes (four rows, one logical pair of chunks each) at a time, and
+// a 32-lane half covers rows {0..3, 8..11} (+4, +32 kk); even swizzle values
+// keep each pair adjacent and give those rows distinct pair positions.
 template <int KCB>
 __device__ __forceinline__ int gemm_b_swz(int r) {
   static_assert(KCB == 8 || KCB == 16 || KCB == 32, "B row chunks");
   if constexpr (KCB >= 16) return (2 * (r & 3)) | (8 * ((r >> 3) & 1));
-  else return (2 * ((r >> 1) & 1)) | (4 * ((r >> 3) & 1));
+  else return 2 * ((r & 3) ^ ((r >> 3) & 1));
 }
 
 __device__ __forceinline__ void barrier_only() {
@@ -77,13 +82,15 @@ __global__ void __launch_bounds__(512) matmul_kernel(const GemmParams p) {
   constexpr int RA = TK * 2, RB = TN * 2;      // row bytes
   constexpr int ATB = TM * RA, BTB = TK * RB, SB = ATB + BTB;
   constexpr int LPA = ATB / (1024 * NW), LPB = BTB / (1024 * NW), LPT = LPA + LPB;
-  constexpr int RPA = 1024 / RA, RPB = 1024 / RB;  // rows per 1 KB block
+  constexpr bool ABLK = KCA == 4;                  // A tile in fragment blocks
+  constexpr int KBA = KCA / 4;                     // A blocks per 16 rows (ABLK)
+  constexpr int RPA = 1024 / RA, RPB = 1024 / RB;  // rows per 1 KB block (row-major)
   constexpr int LEAD = ST - 1;                     // tile j + LEAD is requested in step j
   constexpr int FPK = NNB + NMB, F = KS * FPK;     // operand fragments per k sub-step / step
   constexpr int PF = F < 6 ? F : 6;
   static_assert(TM % (16 * WM) == 0 && TN % (16 * WN) == 0 && TK % 32 == 0, "atom alignment");
   static_assert(ATB % (1024 * NW) == 0 && BTB % (1024 * NW) == 0, "whole copy blocks per wave");
-  static_assert((NW * RPA) % 16 == 0 && (NW * RPB) % 16 == 0, "swizzle period");
+  static_assert((ABLK || (NW * RPA) % 16 == 0) && (NW * RPB) % 16 == 0, "swizzle period");
   static_assert(ST >= 3 && 2 * LPT < 64, "stages and copy counter");
   static_assert(ATB + (TK - 4) * RB + 2 * WTN * WN < 65536, "ds offset range");
 
@@ -118,17 +125,26 @@ __global__ void __launch_bounds__(512) matmul_kernel(const GemmParams p) {
   ATTN_LDS char* const lds = (ATTN_LDS char*)smem;
   const uint32_t lds0 = (uint32_t)(size_t)lds;
 
-  // Copies.  Wave w takes blocks w, w + 8, ... of each tile image; image
-  // slot P of a block holds row P / (chunks per row) at physical chunk
-  // P % (chunks per row), whose logical chunk is that XOR the row's swizzle.
-  // Rows past M and columns past N repeat the last row / column (finite data
-  // whose results are never stored); k chunks past K are clamped too and
-  // their operands zeroed before use.
-  const int ar0 = w * RPA + lane / KCA;
-  const int alc = (lane % KCA) ^ gemm_a_swz<KCA>(ar0);
+  // Copies.  Wave w takes blocks w, w + 8, ... of each tile image, lane l
+  // filling 16-byte slot l of a block.  In fragment blocks (t_K = 32) block
+  // b holds rows 16 b .. +15, slot l row (l % 16) ^ (l / 16), chunk l / 16.
+  // A row-major block holds 1 KB / row bytes rows, slot P at row P / (chunks
+  // per row) and physical chunk P % (chunks per row), whose logical chunk is
+  // that XOR the row's swizzle.  Rows past M and columns past N repeat the
+  // last row / column (finite data whose results are never stored); k chunks
+  // past K are clamped too and their operands zeroed before use.
+  int alc, ar0;
+  if constexpr (ABLK) {
+    alc = lane >> 4;
+    ar0 = 16 * w + ((lane & 15) ^ (lane >> 4));
+  } else {
+    ar0 = w * RPA + lane / KCA;
+    alc = (lane % KCA) ^ gemm_a_swz<KCA>(ar0);
+  }
+  constexpr int ASTEP = ABLK ? 16 * NW : NW * RPA;  // rows between a wave's blocks
   uint32_t aoff[LPA];
 #pragma unroll
-  for (int i = 0; i < LPA; ++i) aoff[i] = (uint32_t)min(ar0 + i * NW * RPA, M - 1 - m0) * (uint32_t)(K * 2);
+  for (int i = 0; i < LPA; ++i) aoff[i] = (uint32_t)min(ar0 + i * ASTEP, M - 1 - m0) * (uint32_t)(K * 2);
   const int br0 = w * RPB + lane / KCB;
   const int blc = (lane % KCB) ^ gemm_b_swz<KCB>(br0);
   const uint32_t bcol = (uint32_t)min(blc, (N - n0) / 8 - 1) * 16;
@@ -149,14 +165,17 @@ __global__ void __launch_bounds__(512) matmul_kernel(const GemmParams p) {
     }
   };
 
-  // Operand fragments.  A^T(kk, mb): row wm WTM + 16 mb + c of the A tile,
-  // logical chunk 4 kk + g.  B^T(kk, nb): rows 32 kk + 8 g + c/4 (+4 for the
-  // upper half) of the B tile, logical chunk (wn WTN + 16 nb)/8 + (c/2)%2,
-  // byte 8 (c%2) within it.  Both swizzles depend only on the lane, and kk,
-  // mb, nb enter the address through disjoint bit fields, so each address is
-  // a lane base XOR a fragment constant plus an immediate row offset.
-  const int sa = gemm_a_swz<KCA>(c);
-  const uint32_t la = (uint32_t)((wm * WTM + c) * RA + 16 * (g ^ sa));
+  // Operand fragments.  A^T(kk, mb): rows wm WTM + 16 mb + c, k chunk
+  // 4 kk + g: in fragment blocks block wm WTM / 16 + mb, slot 16 g + (c ^ g);
+  // row-major, that row at logical chunk 4 kk + g.  B^T(kk, nb): rows
+  // 32 kk + 8 g + c/4 (+4 for the upper half) of the B tile, logical chunk
+  // (wn WTN + 16 nb)/8 + (c/2)%2, byte 8 (c%2) within it.  The swizzles
+  // depend only on the lane, and kk, mb, nb enter the address through
+  // disjoint bit fields, so each address is a lane base XOR a fragment
+  // constant plus an immediate offset.
+  uint32_t la;
+  if constexpr (ABLK) la = (uint32_t)((wm * WTM / 16) * 1024 + 256 * g + 16 * (c ^ g));
+  else la = (uint32_t)((wm * WTM + c) * RA + 16 * (g ^ gemm_a_swz<KCA>(c)));
   const int rb = 8 * g + (c >> 2);
   const int sb = gemm_b_swz<KCB>(rb);
   const uint32_t lb = (uint32_t)(rb * RB + 16 * ((wn * WTN / 8) ^ ((c >> 1) & 1) ^ sb) + 8 * (c & 1));
@@ -168,6 +187,10 @@ __global__ void __launch_bounds__(512) matmul_kernel(const GemmParams p) {
       const i16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4_t*)(base + ATB + (32 * kk + 4) * RB));
       const i16x8_t cat = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
       return __builtin_bit_cast(V8, cat);
+    }
+    if constexpr (ABLK) {
+      ATTN_LDS const char* base = (ATTN_LDS const char*)(size_t)(sbase + la);
+      return __builtin_bit_cast(V8, *(ATTN_LDS const u32x4_t*)(base + (q - NNB) * 1024));
     }
     ATTN_LDS const char* base = (ATTN_LDS const char*)(size_t)(sbase + (la ^ (uint32_t)(64 * kk)));
     return __builtin_bit_cast(V8, *(ATTN_LDS const u32x4_t*)(base + 16 * (q - NNB) * RA));
