@@ -108,6 +108,15 @@ def load():
         return _lib
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
+    # The library needs libamdhip64.so.7, and torch ships its own copy of that
+    # HIP runtime under another file name.  Loaded after torch's, the library
+    # binds to torch's copy and one runtime serves both (torch's streams and
+    # device pointers are valid in its calls); loaded first, it would bring in
+    # the system copy and torch a second one.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(LIB_PATH)
     P = ctypes.POINTER
     sig = {

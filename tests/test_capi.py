@@ -256,3 +256,20 @@ def test_compiled_kernels_fit_without_scratch():
     assert ref["vgpr"] + ref["agpr"] <= capi.attn_vgpr_estimate(hw, atom, op, 32, 64, 8) <= 256
     # one more query block per wave is refused by the count (and would spill)
     assert capi.attn_vgpr_estimate(hw, atom, op, 48, 64, 8) > 256
+
+
+def test_one_hip_runtime_after_load():
+    """Loading the library in a fresh process, before anything imports torch,
+    leaves one HIP runtime mapped: the binding loads torch's copy first, so
+    torch's streams and pointers are valid in the library's calls."""
+    import subprocess
+    import sys
+    code = ("import sys; sys.path.insert(0, %r)\n"
+            "from paper_2609_10937_amd import capi\n"
+            "capi.load()\n"
+            "paths = {l.split()[-1] for l in open('/proc/self/maps') if 'libamdhip64' in l}\n"
+            "print(len(paths)); print(sorted(paths))\n") % ROOT
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
+    assert out.returncode == 0, out.stderr
+    lines = out.stdout.split("\n")
+    assert lines[0] == "1", out.stdout
