@@ -70,9 +70,25 @@ def time_steps(fn, steps, warmup):
     return wall, ev
 
 
+def _time_oracle(A, qh, kh, vh, w, dtype):
+    """Rows of one head timed through the oracle in `dtype`; the sample grows
+    until it is several seconds of work (bounded by the full head)."""
+    A.attention_head(qh, kh, vh, w.scale, w.causal, rows=np.arange(256), dtype=dtype)  # untimed warm-up
+    rows = 1024
+    while True:
+        t0 = time.perf_counter()
+        A.attention_head(qh, kh, vh, w.scale, w.causal, rows=np.arange(rows), dtype=dtype)
+        dt = time.perf_counter() - t0
+        if dt >= 5.0 or rows >= w.L:
+            return rows, dt
+        rows = int(min(w.L, rows * max(2.0, 10.0 / max(dt, 1e-3))))
+        rows = max(1024, rows - rows % 512)
+
+
 def cpu_baseline(w, q, k, v):
     """The oracle as it stands (float64) on the host cores over a bounded sample
-    of the same workload: every key, a contiguous block of query rows."""
+    of the same workload: every key, a contiguous block of query rows.  The
+    same code in float32 is timed beside it."""
     from oracle import attention as A
     try:
         from threadpoolctl import threadpool_info
@@ -82,21 +98,14 @@ def cpu_baseline(w, q, k, v):
     qh = inputs.bits_to_f64(q[0, 0], w.dtype)
     kh = inputs.bits_to_f64(k[0, 0], w.dtype)
     vh = inputs.bits_to_f64(v[0, 0], w.dtype)
-    A.attention_head(qh, kh, vh, w.scale, w.causal, rows=np.arange(256))  # untimed: thread pools, first touch
-    # grow the sample until it is several seconds of work (bounded by the full head)
-    rows = 1024
-    while True:
-        t0 = time.perf_counter()
-        A.attention_head(qh, kh, vh, w.scale, w.causal, rows=np.arange(rows))
-        dt = time.perf_counter() - t0
-        if dt >= 5.0 or rows >= w.L:
-            break
-        rows = int(min(w.L, rows * max(2.0, 10.0 / max(dt, 1e-3))))
-        rows = max(1024, rows - rows % 512)
-    fl = 4.0 * rows * w.L * w.d
+    rows, dt = _time_oracle(A, qh, kh, vh, w, np.float64)
+    rows32, dt32 = _time_oracle(A, qh, kh, vh, w, np.float32)
+    fl, fl32 = 4.0 * rows * w.L * w.d, 4.0 * rows32 * w.L * w.d
     return {"value": fl / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
             "sample": f"float64 oracle, query rows 0..{rows - 1} of {w.L} against all {w.L} keys "
-                      f"(B=1, H=1, d={w.d}), {dt:.2f} s"}
+                      f"(B=1, H=1, d={w.d}), {dt:.2f} s",
+            "fp32": {"value": fl32 / dt32 / 1e12, "unit": "TFLOP/s",
+                     "sample": f"the same oracle in float32, query rows 0..{rows32 - 1}, {dt32:.2f} s"}}
 
 
 def kernel_source_hash():
