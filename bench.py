@@ -203,6 +203,7 @@ def main():
     ap.add_argument("--no-unfused", action="store_true", help="skip the unfused baseline")
     ap.add_argument("--no-sweep", action="store_true", help="skip the sequence-length sweep (Table 3)")
     ap.add_argument("--no-d256", action="store_true", help="skip the head-dimension-256 workloads")
+    ap.add_argument("--no-d96", action="store_true", help="skip the head-dimension-96 workloads")
     ap.add_argument("--no-softmax", action="store_true", help="skip the row-softmax operator")
     ap.add_argument("--no-gemm", action="store_true", help="skip the GEMM operator")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -320,6 +321,24 @@ def main():
             del t3, o3
             torch.cuda.empty_cache()
 
+    d96 = None
+    if not args.no_d96:
+        d96 = []
+        for w3 in inputs.HEAD_DIM_96:
+            print(f"bench: {w3.name}", file=sys.stderr, flush=True)
+            t3 = [upload(x, w3.dtype) for x in inputs.workload_inputs(w3)]
+            o3 = torch.empty_like(t3[0])
+            n3 = 20 if w3.B * w3.H == 1 else 5
+            _, ev3 = time_steps(lambda: capi.attn_fwd(t3[0], t3[1], t3[2], o3, w3.scale, w3.causal), n3, n3)
+            p3 = capi.attn_fwd_plan(w3.B, w3.H, w3.L, w3.d, w3.causal, capi.ATTN_BF16)
+            d96.append({"workload": w3.name, "ms": round(ev3, 4),
+                         "tflops": round(flops(w3) / (ev3 * 1e-3) / 1e12, 1),
+                         "pct_peak": round(100 * flops(w3) / (ev3 * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 1),
+                         "tiles": {"t_kv": p3.t_kv, "t_q_wave": p3.t_q_wave, "n_waves": p3.n_waves,
+                                   "n_split": p3.n_split, "grid": p3.grid}})
+            del t3, o3
+            torch.cuda.empty_cache()
+
     smx = None
     if not args.no_softmax:
         # The row-softmax operator of Section 4.3: the paper's 512 x 512 and the
@@ -418,6 +437,7 @@ def main():
         "secondary": secondary,
         "l_sweep": sweep,
         "head_dim_256": d256,
+        "head_dim_96": d96,
         "softmax": smx,
         "gemm": gemm,
         "cpu_baseline": cpu,

@@ -20,7 +20,7 @@
  *    enqueue work on `stream` (a hipStream_t; NULL is the null stream) and
  *    return without synchronising.  Inputs must stay valid until that work
  *    completes.
- *  - Sizes: 1 <= B, H; 1 <= L <= ATTN_MAX_L; d in {64, 128, 256};
+ *  - Sizes: 1 <= B, H; 1 <= L <= ATTN_MAX_L; d in {64, 96, 128, 256};
  *    L * d * 2 <= 2^32 (one head's Q, K or V within 4 GiB: L <= 2^23 at
  *    d = 256); B * H * L * d < 2^62.
  */
@@ -42,7 +42,7 @@ typedef enum {
   ATTN_OK = 0,
   ATTN_E_NULLPTR = -1,        /* a required pointer is NULL */
   ATTN_E_SHAPE = -2,          /* B, H or L outside the supported range */
-  ATTN_E_UNSUPPORTED_D = -3,  /* head dimension not in {64, 128, 256} */
+  ATTN_E_UNSUPPORTED_D = -3,  /* head dimension not in {64, 96, 128, 256} */
   ATTN_E_DTYPE = -4,          /* dtype not an attn_dtype_t */
   ATTN_E_ALIGN = -5,          /* a tensor base address is not 16-byte aligned */
   ATTN_E_INFEASIBLE = -6,     /* tile derivation found no feasible tile (report.binding says why) */

@@ -34,6 +34,8 @@ SOURCES = [
     "fwd_f16_d128.hip",
     "fwd_bf16_d256.hip",
     "fwd_f16_d256.hip",
+    "fwd_bf16_d96.hip",
+    "fwd_f16_d96.hip",
     "gemm_bf16.hip",
     "gemm_f16.hip",
 ]

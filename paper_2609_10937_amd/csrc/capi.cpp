@@ -18,6 +18,8 @@ const FwdInstance* fwd_instances_f16_d64(int* n);
 const FwdInstance* fwd_instances_f16_d128(int* n);
 const FwdInstance* fwd_instances_bf16_d256(int* n);
 const FwdInstance* fwd_instances_f16_d256(int* n);
+const FwdInstance* fwd_instances_bf16_d96(int* n);
+const FwdInstance* fwd_instances_f16_d96(int* n);
 }  // namespace attn
 
 using namespace attn;
@@ -39,7 +41,7 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 int check_shape(int B, int H, int L, int d, int dtype) {
   if (B <= 0 || H <= 0 || L <= 0 || L > ATTN_MAX_L) return ATTN_E_SHAPE;
-  if (d != 64 && d != 128 && d != 256) return ATTN_E_UNSUPPORTED_D;
+  if (d != 64 && d != 96 && d != 128 && d != 256) return ATTN_E_UNSUPPORTED_D;
   if ((int64_t)L * d * 2 > (int64_t(1) << 32)) return ATTN_E_SHAPE;  // byte offsets within a head are 32-bit
   if (dtype != ATTN_BF16 && dtype != ATTN_F16) return ATTN_E_DTYPE;
   const long double elems = (long double)B * H * L * d;
@@ -97,8 +99,8 @@ std::map<int, DeviceState> g_dev;
 
 const FwdInstance* find_instance(int dtype, int d, int t_kv, int q_blocks, int n_waves) {
   using Fn = const FwdInstance* (*)(int*);
-  Fn fns[] = {fwd_instances_bf16_d64, fwd_instances_bf16_d128, fwd_instances_bf16_d256,
-              fwd_instances_f16_d64,  fwd_instances_f16_d128,  fwd_instances_f16_d256};
+  Fn fns[] = {fwd_instances_bf16_d64, fwd_instances_bf16_d96, fwd_instances_bf16_d128, fwd_instances_bf16_d256,
+              fwd_instances_f16_d64,  fwd_instances_f16_d96,  fwd_instances_f16_d128,  fwd_instances_f16_d256};
   for (Fn f : fns) {
     int n = 0;
     const FwdInstance* t = f(&n);
@@ -229,7 +231,7 @@ const char* attn_strerror(int status) {
     case ATTN_OK: return "ok";
     case ATTN_E_NULLPTR: return "null pointer argument";
     case ATTN_E_SHAPE: return "B, H or L out of range";
-    case ATTN_E_UNSUPPORTED_D: return "head dimension must be 64 or 128";
+    case ATTN_E_UNSUPPORTED_D: return "head dimension must be 64, 96, 128 or 256";
     case ATTN_E_DTYPE: return "dtype must be ATTN_BF16 or ATTN_F16";
     case ATTN_E_ALIGN: return "tensor base address not 16-byte aligned";
     case ATTN_E_INFEASIBLE: return "tile derivation infeasible";

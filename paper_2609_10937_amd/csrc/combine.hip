@@ -46,10 +46,12 @@ hipError_t launch_combine(const FwdParams& p, int d, int dtype, hipStream_t s) {
   if (dtype == ATTN_BF16) {
     if (d == 256) hipLaunchKernelGGL((combine_kernel<ATTN_BF16, 256>), dim3(grid), dim3(256), 0, s, p);
     else if (d == 128) hipLaunchKernelGGL((combine_kernel<ATTN_BF16, 128>), dim3(grid), dim3(256), 0, s, p);
+    else if (d == 96) hipLaunchKernelGGL((combine_kernel<ATTN_BF16, 96>), dim3(grid), dim3(256), 0, s, p);
     else hipLaunchKernelGGL((combine_kernel<ATTN_BF16, 64>), dim3(grid), dim3(256), 0, s, p);
   } else {
     if (d == 256) hipLaunchKernelGGL((combine_kernel<ATTN_F16, 256>), dim3(grid), dim3(256), 0, s, p);
     else if (d == 128) hipLaunchKernelGGL((combine_kernel<ATTN_F16, 128>), dim3(grid), dim3(256), 0, s, p);
+    else if (d == 96) hipLaunchKernelGGL((combine_kernel<ATTN_F16, 96>), dim3(grid), dim3(256), 0, s, p);
     else hipLaunchKernelGGL((combine_kernel<ATTN_F16, 64>), dim3(grid), dim3(256), 0, s, p);
   }
   return hipGetLastError();

@@ -298,12 +298,17 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   constexpr int NKB = TKV / 16;             // 16-key blocks of S^T
   constexpr int NP = TKV / 32;              // k steps of GEMM2
   constexpr int NDB = D / 16;               // 16-row blocks of O^T
-  constexpr int KCH = D / 8;                // 16-byte chunks per row
-  constexpr int TILE = TKV * D;             // elements of one K or V tile
+  // K/V rows in LDS hold DL elements: d itself when a power of two, else the
+  // next power of two (d = 96 -> 128), the chunks past d copies of the last
+  // one that no product reads, so every swizzle and copy pattern is the
+  // power-of-two one.
+  constexpr int DL = (D & (D - 1)) == 0 ? D : (D <= 128 ? 128 : 256);
+  constexpr int KCH = DL / 8;               // 16-byte chunks per LDS row
+  constexpr int TILE = TKV * DL;            // elements of one K or V tile in LDS
   constexpr int CHUNKS = TKV * KCH;
   constexpr int NCW = NW;                   // waves that copy tiles (all)
   constexpr int LPW = CHUNKS / (NCW * 64);  // 1 KB copies per copying wave per tile and tensor
-  static_assert(TKV % 32 == 0 && D % 32 == 0 && KCH >= 8 && (KCH & (KCH - 1)) == 0, "tile alignment");
+  static_assert(TKV % 32 == 0 && D % 32 == 0 && D <= DL && KCH >= 8 && (KCH & (KCH - 1)) == 0, "tile alignment");
   static_assert(CHUNKS % (NCW * 64) == 0, "tile copies must split evenly across waves");
   // Tiles requested ahead.  In M(j) a wave requests its part of tile
   // j + 1 + AHEAD, whose stage held tile j + 1 + AHEAD - ST; that V tile is
@@ -376,9 +381,10 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   const int n = min(n_kv, t_begin + p.tiles_per_split) - t_begin;  // tiles of this workgroup
 
   // LDS image: stage st holds the K tile at byte st*STAGEB and the V tile
-  // TILEB after it, each row-major [TKV][D] in 16-byte chunks, chunk
+  // TILEB after it, each row-major [TKV][DL] in 16-byte chunks, chunk
   // positions XOR-swizzled per row (k_swz / v_swz).
-  constexpr int ROWB = D * 2;               // bytes per K/V row
+  constexpr int ROWB = DL * 2;              // bytes per K/V row in LDS
+  constexpr int GROWB = D * 2;              // bytes per K/V row in HBM
   constexpr int TILEB = TKV * ROWB;         // bytes per K or V tile
   constexpr int STAGEB = 2 * TILEB;
   ATTN_LDS char* const lds = (ATTN_LDS char*)smem;
@@ -405,8 +411,13 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
 #pragma unroll
   for (int i = 0; i < NCB; ++i) {
     const int r = (int)r0 + i * NCW * RPB, pc = lane % KCH;
-    kcb[i] = (uint32_t)((pc ^ k_swz<KCH>(r)) * 16);
-    vcb[i] = (uint32_t)((pc ^ v_swz<KCH>(r)) * 16);
+    if constexpr (D == DL) {
+      kcb[i] = (uint32_t)((pc ^ k_swz<KCH>(r)) * 16);
+      vcb[i] = (uint32_t)((pc ^ v_swz<KCH>(r)) * 16);
+    } else {
+      kcb[i] = (uint32_t)(min(pc ^ k_swz<KCH>(r), D / 8 - 1) * 16);
+      vcb[i] = (uint32_t)(min(pc ^ v_swz<KCH>(r), D / 8 - 1) * 16);
+    }
   }
   // This wave's part of tile j: its LPW blocks of the K image and of the V
   // image, as copies 0 .. NC-1 (copy 2i is block i of K, 2i+1 block i of V);
@@ -421,8 +432,8 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
     for (int ci = lo; ci < hi; ++ci) {
       const int i = ci >> 1;
       const uint32_t row = min(t + (uint32_t)(i * NCW * RPB), (uint32_t)(L - 1));
-      if (ci & 1) copy_to_lds(Vh, row * ROWB + vcb[SHIFT ? 0 : i], kdst + TILEB + i * NCW * 1024);
-      else copy_to_lds(Kh, row * ROWB + kcb[SHIFT ? 0 : i], kdst + i * NCW * 1024);
+      if (ci & 1) copy_to_lds(Vh, row * GROWB + vcb[SHIFT ? 0 : i], kdst + TILEB + i * NCW * 1024);
+      else copy_to_lds(Kh, row * GROWB + kcb[SHIFT ? 0 : i], kdst + i * NCW * 1024);
     }
   };
   // This wave's copies of tile j are complete once no more than the copies
@@ -653,7 +664,10 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const float lt = lacc[qb][0];
-    const int q = q0 + 16 * qb + c;
+    int q = q0 + 16 * qb + c;
+    // Row offsets at a d that is not a power of two are multiplications: keep
+    // the compiler from carrying the Q loads' ones through the loop.
+    if constexpr (D != DL) asm volatile("" : "+v"(q));
     if (p.n_split == 1) {
       const float inv = lt > 0.f ? 1.f / lt : 0.f;
       if (q < L) {

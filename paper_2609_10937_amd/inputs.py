@@ -71,6 +71,14 @@ HEAD_DIM_256 = (
 )
 WORKLOADS.update({w.name: w for w in HEAD_DIM_256})
 
+# Head dimension 96 (t_kv = 64, 48 rows per wave): the same two shapes as the
+# d = 128 headline and batched causal workloads.
+HEAD_DIM_96 = (
+    Workload("single_head_l16384_d96", 1, 1, 16384, 96, "bf16", False, 1.0, 1211),
+    Workload("causal_b4h32_l16384_d96", 4, 32, 16384, 96, "bf16", True, 1.0, 1212),
+)
+WORKLOADS.update({w.name: w for w in HEAD_DIM_96})
+
 
 def softmax_scale(d: int) -> float:
     """1/sqrt(d) evaluated in float32, returned as the Python float of that value."""

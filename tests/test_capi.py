@@ -126,7 +126,7 @@ def test_fused_structure_plans_every_shape():
     """Every shape the API accepts maps to a compiled instance on the gfx950 descriptor."""
     hw = capi.attn_hw_desc_preset("gfx950")
     shapes = [(w.B, w.H, w.L, w.d, w.causal) for w in inputs.WORKLOADS.values()]
-    for d in (64, 128, 256):
+    for d in (64, 96, 128, 256):
         for L in (1, 2, 15, 16, 17, 31, 33, 63, 64, 65, 100, 127, 129, 159, 161, 1000, 1023, 4097,
                   16384, 65536, 1 << 20, capi.ATTN_MAX_L):
             for B, H in ((1, 1), (1, 3), (2, 8), (4, 32), (64, 64)):
@@ -141,7 +141,7 @@ def test_fused_structure_plans_every_shape():
             assert r.feasible and r.grid >= 1
             assert r.vgpr_est <= r.vgpr_budget and r.lds_used <= r.lds_budget
             seen.add((d, r.t_kv, r.t_q_wave, r.n_waves))
-    assert (128, 64, 32, 8) in seen and (256, 32, 16, 8) in seen
+    assert (128, 64, 32, 8) in seen and (256, 32, 16, 8) in seen and (96, 64, 48, 8) in seen
 
 
 def test_head_bytes_fit_32_bit_offsets():
@@ -177,7 +177,7 @@ def _fwd(lib, q=P, k=P, v=P, o=P, B=1, H=1, L=16, d=64, scale=0.125, causal=0, d
     (dict(q=None), "ATTN_E_NULLPTR"), (dict(o=None), "ATTN_E_NULLPTR"),
     (dict(k=P + 8), "ATTN_E_ALIGN"), (dict(v=P + 2), "ATTN_E_ALIGN"),
     (dict(B=0), "ATTN_E_SHAPE"), (dict(H=-1), "ATTN_E_SHAPE"), (dict(L=0), "ATTN_E_SHAPE"),
-    (dict(L=(1 << 24) + 1), "ATTN_E_SHAPE"), (dict(d=96), "ATTN_E_UNSUPPORTED_D"),
+    (dict(L=(1 << 24) + 1), "ATTN_E_SHAPE"), (dict(d=80), "ATTN_E_UNSUPPORTED_D"),
     (dict(d=0), "ATTN_E_UNSUPPORTED_D"), (dict(dtype=2), "ATTN_E_DTYPE"),
     (dict(scale=-1.0), "ATTN_E_SCALE"), (dict(scale=float("nan")), "ATTN_E_SCALE"),
     (dict(scale=float("inf")), "ATTN_E_SCALE"),
@@ -201,7 +201,7 @@ def test_unfused_rejects_bad_arguments(lib):
 def test_partial_and_merge_reject_bad_arguments(lib):
     f = lib.attn_fwd_partial
     assert f(None, P, P, P, 1, 1, 16, 64, 0.1, 0, 0, None, 0, None) == capi.CODE["ATTN_E_NULLPTR"]
-    assert f(P, P, P, P, 1, 1, 16, 96, 0.1, 0, 0, None, 0, None) == capi.CODE["ATTN_E_UNSUPPORTED_D"]
+    assert f(P, P, P, P, 1, 1, 16, 80, 0.1, 0, 0, None, 0, None) == capi.CODE["ATTN_E_UNSUPPORTED_D"]
     assert f(P, P, P, P, 1, 1, 16, 64, -0.1, 0, 0, None, 0, None) == capi.CODE["ATTN_E_SCALE"]
     g = lib.attn_fwd_merge
     assert g(None, 0, None, 1, 1, 16, 64, 0.1, 0, 0, None) == capi.CODE["ATTN_E_NULLPTR"]
@@ -240,7 +240,7 @@ def test_compiled_kernels_fit_without_scratch():
     with open(path) as f:
         res = json.load(f)
     fwd = {k: v for k, v in res.items() if "fwd_kernel" in k}
-    assert len(fwd) == 28
+    assert len(fwd) == 40
     for name, r in res.items():
         assert r["scratch"] == 0, name
     for name, r in fwd.items():

@@ -129,7 +129,7 @@ def test_sweep_l32768_sampled_rows():
 
 # ------------------------------------------------------------ edge shapes
 
-EDGE = [(L, d, causal, dt) for L in (1, 17, 100, 1000, 4097) for d in (64, 128, 256)
+EDGE = [(L, d, causal, dt) for L in (1, 17, 100, 1000, 4097) for d in (64, 96, 128, 256)
         for causal in (False, True) for dt in ("bf16", "f16")]
 
 
@@ -157,6 +157,30 @@ def test_head_dim_256_all_rows(B, H, L, causal, dtype):
     ref = A.attention(_f64(q, dtype), _f64(k, dtype), _f64(v, dtype), s, causal)
     mx, mn = _gpu.assert_close(_gpu.download(o, dtype), ref, dtype, f"d256 L{L}")
     print(f"  d256 L{L}: max_abs {mx:.3e} mean_abs {mn:.3e}", flush=True)
+
+
+# (B, H, L, causal, dtype) -> the (rows per wave, waves) instance the derivation picks
+D96 = [((2, 8, 2048, True, "bf16"), (48, 8)), ((1, 4, 1000, False, "f16"), (48, 4)),
+       ((1, 2, 1000, True, "bf16"), (48, 2)), ((4, 32, 63, False, "bf16"), (48, 1)),
+       ((2, 8, 161, True, "f16"), (32, 1)), ((1, 1, 100, False, "bf16"), (16, 1)),
+       ((1, 1, 8192, False, "bf16"), (48, 8))]
+
+
+@pytest.mark.parametrize("case,instance", D96)
+def test_head_dim_96_all_rows(case, instance):
+    """d = 96 (t_kv = 64, K/V rows padded to 128 elements in LDS): all rows
+    against the oracle, one case per compiled instance; the single-head case
+    runs with 16 key-range splits."""
+    B, H, L, causal, dtype = case
+    r = capi.attn_fwd_plan(B, H, L, 96, causal, capi.ATTN_BF16 if dtype == "bf16" else capi.ATTN_F16)
+    assert (r.t_q_wave, r.n_waves) == instance
+    print(f"case d96 B{B} H{H} L{L} causal{int(causal)} {dtype} instance {instance}", flush=True)
+    q, k, v = inputs.make_qkv(B, H, L, 96, dtype, seed=L + 96)
+    s = inputs.softmax_scale(96)
+    o = _gpu.fused(_gpu.upload(q, dtype), _gpu.upload(k, dtype), _gpu.upload(v, dtype), s, causal)
+    ref = A.attention(_f64(q, dtype), _f64(k, dtype), _f64(v, dtype), s, causal)
+    mx, mn = _gpu.assert_close(_gpu.download(o, dtype), ref, dtype, f"d96 L{L}")
+    print(f"  d96 L{L}: max_abs {mx:.3e} mean_abs {mn:.3e}", flush=True)
 
 
 @pytest.mark.parametrize("causal", [False, True])
