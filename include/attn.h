@@ -112,8 +112,9 @@ typedef struct {
 } attn_tile_report_t;
 
 /* Fill `out` with a named descriptor: "paper_gpu_a" and "paper_gpu_b" (the two
- * CDNA descriptors of Section 3), or "gfx950" (MI355X public figures).
- * ATTN_E_ARG for an unknown name. */
+ * CDNA descriptors of Section 3), "gfx950" (MI355X public figures) or
+ * "gfx942" (MI300X public figures; for the derivation only: the kernels are
+ * built for gfx950).  ATTN_E_ARG for an unknown name. */
 int attn_hw_desc_preset(const char* name, attn_hw_desc_t* out);
 
 /* Descriptor of HIP device `device`: CU count, LDS size, wavefront size and
@@ -121,7 +122,8 @@ int attn_hw_desc_preset(const char* name, attn_hw_desc_t* out);
  * the device is not gfx950, ATTN_E_HIP if the runtime cannot be queried. */
 int attn_hw_desc_query(int device, attn_hw_desc_t* out);
 
-/* Named atoms: "f32_16x16x4" (the paper's), "bf16_16x16x32", "f16_16x16x32". */
+/* Named atoms: "f32_16x16x4" (the paper's), "bf16_16x16x32", "f16_16x16x32"
+ * (gfx950), "bf16_16x16x16", "f16_16x16x16" (gfx942). */
 int attn_atom_preset(const char* name, attn_mfma_atom_t* out);
 
 /* Fill `out` with the operation (B, H, L, d, dtype, causal) and the structure

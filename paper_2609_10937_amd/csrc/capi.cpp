@@ -251,6 +251,24 @@ int attn_hw_desc_preset(const char* name, attn_hw_desc_t* out) {
     gfx950_desc(out);
     return ATTN_OK;
   }
+  if (strcmp(name, "gfx942") == 0) {
+    // MI300X public figures: 304 CUs, 64 KiB LDS, 512 registers per lane at one
+    // wave per SIMD, dense bf16 1307.4 TFLOP/s at 2.1 GHz (2048 per clock per
+    // CU, on the 16x16x16 atom), 5.3 TB/s.
+    memset(out, 0, sizeof(*out));
+    out->lds_bytes = 64 * 1024;
+    out->vgpr_per_thread = 512;
+    out->wavefront_size = 64;
+    out->num_cus = 304;
+    out->simds_per_cu = 4;
+    out->lds_bytes_per_clk = 128;
+    out->mfma_flops_per_clk_cu = 2048;
+    out->hbm_tbps = 5.3;
+    out->peak_tflops = 1307.4;
+    out->clock_ghz = 2.1;
+    fill_name(out, "gfx942");
+    return ATTN_OK;
+  }
   const bool a = strcmp(name, "paper_gpu_a") == 0, b = strcmp(name, "paper_gpu_b") == 0;
   if (!a && !b) return ATTN_E_ARG;
   // Section 3, the two CDNA descriptors of the listing.
@@ -280,6 +298,10 @@ int attn_atom_preset(const char* name, attn_mfma_atom_t* out) {
   }
   if (strcmp(name, "bf16_16x16x32") == 0 || strcmp(name, "f16_16x16x32") == 0) {
     *out = {16, 16, 32, 2, 4};
+    return ATTN_OK;
+  }
+  if (strcmp(name, "bf16_16x16x16") == 0 || strcmp(name, "f16_16x16x16") == 0) {  // gfx942's 16-bit atom
+    *out = {16, 16, 16, 2, 4};
     return ATTN_OK;
   }
   return ATTN_E_ARG;

@@ -40,7 +40,7 @@ def test_presets():
     b = capi.attn_hw_desc_preset("paper_gpu_b")
     assert (a.num_cus, b.num_cus, a.lds_bytes, a.vgpr_per_thread) == (120, 304, 65536, 256)
     with pytest.raises(capi.AttnError) as e:
-        capi.attn_hw_desc_preset("gfx942")
+        capi.attn_hw_desc_preset("gfx908")
     assert e.value.status == capi.CODE["ATTN_E_ARG"]
     at = capi.attn_atom_preset("f32_16x16x4")
     assert (at.m, at.n, at.k, at.in_bytes, at.acc_bytes) == (16, 16, 4, 4, 4)
@@ -273,3 +273,27 @@ def test_one_hip_runtime_after_load():
     assert out.returncode == 0, out.stderr
     lines = out.stdout.split("\n")
     assert lines[0] == "1", out.stdout
+
+
+def test_gfx942_class_descriptor():
+    """The derivation on MI300X's published figures (64 KiB LDS, 512 registers,
+    304 CUs, the 16x16x16 atom) for this library's kernel structures: the ten
+    staged K/V tiles leave t_kv = floor(65536 / (10 * 128 * 2)) = 25 -> 16 at
+    d = 128 and nothing at d = 256; the GEMM's five stages of 1 KB copy blocks
+    leave no t_K.  A port needs fewer stages; the kernels are built for gfx950."""
+    hw = capi.attn_hw_desc_preset("gfx942")
+    assert (hw.lds_bytes, hw.vgpr_per_thread, hw.num_cus, hw.name) == (65536, 512, 304, b"gfx942")
+    atom = capi.attn_atom_preset("bf16_16x16x16")
+    assert (atom.m, atom.n, atom.k) == (16, 16, 16)
+    op = capi.attn_fwd_op(1, 1, 16384, 128, 0, capi.ATTN_BF16)
+    rc, r = capi.attn_tile_derive(hw, atom, op)
+    assert rc == 0 and r.t_kv == 16 and r.lds_used == 10 * 16 * 128 * 2 and r.grid >= hw.num_cus
+    assert r.vgpr_est <= r.vgpr_budget == 256
+    op = capi.attn_fwd_op(1, 1, 16384, 256, 0, capi.ATTN_BF16)
+    rc, r = capi.attn_tile_derive(hw, atom, op)
+    assert rc == capi.CODE["ATTN_E_INFEASIBLE"] and r.binding == b"LDS"
+    with pytest.raises(capi.AttnError) as e:
+        capi.attn_gemm_derive(hw, atom, 4096, 4096, 4096)
+    assert e.value.status == capi.CODE["ATTN_E_INFEASIBLE"]
+    with pytest.raises(capi.AttnError):
+        capi.attn_hw_desc_preset("gfx90x")
