@@ -29,6 +29,7 @@ WORKLOAD = "single_head_l16384_d128"
 SECONDARY = "causal_b4h32_l16384_d128"
 METRIC = "fused attention fwd TFLOPS (% bf16 MFMA peak) + HBM bytes vs unfused, L=16384 d=128"
 PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 matrix-core peak
+PEAK_F32_MFMA_TFLOPS = 157.3  # MI355X dense fp32 matrix-core peak
 HBM_TBPS = 8.0
 
 
@@ -391,6 +392,24 @@ def main():
                           "warp_n": rep.warp_n, "grid": rep.grid, "vgpr_est": rep.vgpr_est,
                           "binding": rep.binding.decode()}}
         del ga, gb, gc
+        # The same shape in fp32 (the section's type: 12.3 TFLOP/s = 53% of its GPU's
+        # fp32 matrix peak) on the fp32 family's tiles, against MI355X's fp32 matrix peak.
+        rep32 = capi.attn_gemm_derive(hwq, capi.attn_atom_preset("f32_16x16x4"), M, N, K)
+        fa = torch.from_numpy(inputs.make_matrix_f32(M, K, seed=1403)).cuda()
+        fb = torch.from_numpy(inputs.make_matrix_f32(K, N, seed=1404)).cuda()
+        fc = torch.empty((M, N), dtype=torch.float32, device="cuda")
+        _, f_ms = time_steps(lambda: capi.attn_gemm(fa, fb, fc), 20, 20)
+        _, tf_ms = time_steps(lambda: torch.mm(fa, fb), 20, 20)
+        gemm["fp32"] = {"us": round(1e3 * f_ms, 2), "tflops": round(gfl / (f_ms * 1e-3) / 1e12, 1),
+                        "peak": PEAK_F32_MFMA_TFLOPS,
+                        "frac_peak": round(gfl / (f_ms * 1e-3) / 1e12 / PEAK_F32_MFMA_TFLOPS, 4),
+                        "paper": {"tflops": 12.3, "frac_peak": 0.53, "peak": 23.1},
+                        "torch_mm_fp32_us": round(1e3 * tf_ms, 2),
+                        "torch_mm_tflops": round(gfl / (tf_ms * 1e-3) / 1e12, 1),
+                        "tiles": {"t_m": rep32.t_m, "t_n": rep32.t_n, "t_k": rep32.t_k, "warp_m": rep32.warp_m,
+                                  "warp_n": rep32.warp_n, "grid": rep32.grid, "vgpr_est": rep32.vgpr_est,
+                                  "binding": rep32.binding.decode()}}
+        del fa, fb, fc
         torch.cuda.empty_cache()
 
     cpu = None

@@ -36,7 +36,7 @@ extern "C" {
 
 #define ATTN_MAX_L (1 << 24)
 
-typedef enum { ATTN_BF16 = 0, ATTN_F16 = 1 } attn_dtype_t;
+typedef enum { ATTN_BF16 = 0, ATTN_F16 = 1, ATTN_F32 = 2 /* attn_gemm only */ } attn_dtype_t;
 
 typedef enum {
   ATTN_OK = 0,
@@ -232,15 +232,17 @@ int attn_softmax(const void* X, void* Y, int64_t rows, int64_t n, int causal, in
 
 /* GEMM C = A B (Section 4's worked example, Figure 1): workgroup tile
  * t_M x t_N x t_K and per-wave tile from the same closed-form rules as the
- * attention tiles, for the GEMM kernel's fixed structure (5 LDS stages of an
- * A and a B tile, 2 x 4 waves, 2 waves per SIMD):
+ * attention tiles, for the fixed structure of the kernel family that runs the
+ * atom (16-bit atoms: 5 LDS stages of an A and a B tile, 2 x 4 waves, 2 waves
+ * per SIMD; 4-byte atoms: 3 stages, 2 x 2 waves, 1 wave per SIMD):
  *   LDS      t_M = t_N = floor(sqrt(LDS / elem)), aligned down to the atom
  *            times the waves along each side; t_K = floor(LDS / (stages
  *            (t_M + t_N) elem)), aligned down to the atom's k and to whole
  *            1 KB copy blocks per wave;
- *   VGPR     the per-wave accumulators, (t_M / 2)(t_N / 4) fp32 values over
- *            the wavefront, plus the fixed registers within the budget at
- *            2 waves per SIMD (the larger side halves until they fit);
+ *   VGPR     the per-wave accumulators, (t_M / W_M)(t_N / W_N) fp32 values
+ *            over the wavefront, plus the fixed registers within the budget
+ *            at the family's waves per SIMD (the larger side halves until
+ *            they fit);
  *   CU count while ceil(M / t_M) ceil(N / t_N) is below the CU count the
  *            larger side halves, down to one atom per wave.
  * Section 4 prints the LDS rule with LDS / 2 under the square root; the
@@ -265,12 +267,15 @@ typedef struct {
 int attn_gemm_derive(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, int64_t M, int64_t N, int64_t K,
                      attn_gemm_report_t* out);
 
-/* C = A B on the matrix cores: A [M][K] and B [K][N] row-major in `dtype`
- * (bf16 or f16), C [M][N] row-major fp32, every product and sum in fp32
- * (Section 4: the GEMM validated against a double-precision reference).
- * Tiles come from attn_gemm_derive on the current device's descriptor.
- * Sizes: 1 <= M < 2^31; 8 <= N <= 2^24 and 8 <= K <= 2^22, both multiples of
- * 8 (ATTN_E_SHAPE otherwise); A, B and C 16-byte aligned (ATTN_E_ALIGN).  C
+/* C = A B on the matrix cores: A [M][K] and B [K][N] row-major in `dtype`,
+ * C [M][N] row-major fp32, every sum in fp32 (Section 4: the GEMM validated
+ * against a double-precision reference).  bf16/f16 inputs run on the 16x16x32
+ * atom (products exact in fp32), fp32 inputs (ATTN_F32, the section's own
+ * type) on the 16x16x4 fp32 atom, each with its kernel family's tiles from
+ * attn_gemm_derive on the current device's descriptor.
+ * Sizes: 1 <= M < 2^31; N and K multiples of 8 (bf16/f16) or 4 (fp32), at
+ * least that, K <= 2^22 and N <= 2^24 (bf16/f16) or 2^22 (fp32)
+ * (ATTN_E_SHAPE otherwise); A, B and C 16-byte aligned (ATTN_E_ALIGN).  C
  * must not overlap A or B.  Asynchronous on `stream`. */
 int attn_gemm(const void* A, const void* B, float* C, int64_t M, int64_t N, int64_t K, int dtype, void* stream);
 

@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(HERE, "libattn.so")
 
 ATTN_BF16 = 0
 ATTN_F16 = 1
+ATTN_F32 = 2  # attn_gemm only
 ATTN_MAX_L = 1 << 24
 
 STATUS = {
@@ -316,8 +317,9 @@ def attn_gemm_derive(hw: HwDesc, atom: Atom, M: int, N: int, K: int) -> GemmRepo
 
 
 def attn_gemm(a, b, c, stream=None):
-    """c = a @ b: a [M, K] and b [K, N] contiguous bf16 or f16 device tensors of one
-    dtype, c [M, N] contiguous float32."""
+    """c = a @ b: a [M, K] and b [K, N] contiguous device tensors of one dtype
+    (bf16, f16 or float32), c [M, N] contiguous float32."""
+    import torch
     if a.dim() != 2 or b.dim() != 2 or c.dim() != 2:
         raise AttnError(CODE["ATTN_E_SHAPE"], "a, b and c must be matrices")
     M, K = a.shape
@@ -325,8 +327,7 @@ def attn_gemm(a, b, c, stream=None):
         raise AttnError(CODE["ATTN_E_SHAPE"], f"shapes {tuple(a.shape)} @ {tuple(b.shape)} -> {tuple(c.shape)}")
     if b.dtype != a.dtype:
         raise AttnError(CODE["ATTN_E_DTYPE"], "a and b must share a dtype")
-    import torch
     if c.dtype != torch.float32:
         raise AttnError(CODE["ATTN_E_DTYPE"], "c must be float32")
-    _check(load().attn_gemm(_dev_ptr(a), _dev_ptr(b), _dev_ptr(c), M, b.shape[1], K, dtype_code(a),
-                            _stream_ptr(a, stream)))
+    code = ATTN_F32 if a.dtype == torch.float32 else dtype_code(a)
+    _check(load().attn_gemm(_dev_ptr(a), _dev_ptr(b), _dev_ptr(c), M, b.shape[1], K, code, _stream_ptr(a, stream)))

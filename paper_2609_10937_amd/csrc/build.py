@@ -38,6 +38,7 @@ SOURCES = [
     "fwd_f16_d96.hip",
     "gemm_bf16.hip",
     "gemm_f16.hip",
+    "gemm_f32.hip",
 ]
 
 ARCH = "gfx950"

@@ -477,11 +477,13 @@ int attn_gemm_derive(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, int
 
 int attn_gemm(const void* A, const void* B, float* C, int64_t M, int64_t N, int64_t K, int dtype, void* stream) {
   if (!A || !B || !C) return ATTN_E_NULLPTR;
-  if (dtype != ATTN_BF16 && dtype != ATTN_F16) return ATTN_E_DTYPE;
-  // 32-bit lane offsets within a workgroup's panels: t_M K 2 and t_K N 2
-  // bytes stay below 2^32 for K <= 2^22 and N <= 2^24.
-  if (M < 1 || M > 0x7fffffffLL || N < 8 || N > (int64_t(1) << 24) || N % 8 != 0 || K < 8 ||
-      K > (int64_t(1) << 22) || K % 8 != 0)
+  if (dtype != ATTN_BF16 && dtype != ATTN_F16 && dtype != ATTN_F32) return ATTN_E_DTYPE;
+  // Whole 16-byte chunks along N and K; 32-bit lane offsets within a
+  // workgroup's panels (t_M K e and t_K N e bytes below 2^32).
+  const int64_t per_chunk = dtype == ATTN_F32 ? 4 : 8;
+  const int64_t max_n = dtype == ATTN_F32 ? (int64_t(1) << 22) : (int64_t(1) << 24);
+  if (M < 1 || M > 0x7fffffffLL || N < per_chunk || N > max_n || N % per_chunk != 0 || K < per_chunk ||
+      K > (int64_t(1) << 22) || K % per_chunk != 0)
     return ATTN_E_SHAPE;
   if (!aligned16(A) || !aligned16(B) || !aligned16(C)) return ATTN_E_ALIGN;
   int dev = 0;
@@ -489,7 +491,7 @@ int attn_gemm(const void* A, const void* B, float* C, int64_t M, int64_t N, int6
   attn_hw_desc_t desc;
   int rc = device_desc(dev, &desc);
   if (rc != ATTN_OK) return rc;
-  const attn_mfma_atom_t atom = {16, 16, 32, 2, 4};
+  const attn_mfma_atom_t atom = dtype == ATTN_F32 ? attn_mfma_atom_t{16, 16, 4, 4, 4} : attn_mfma_atom_t{16, 16, 32, 2, 4};
   attn_gemm_report_t rep;
   rc = derive_gemm(&desc, &atom, M, N, K, &rep);
   if (rc != ATTN_OK) return rc;
@@ -497,7 +499,9 @@ int attn_gemm(const void* A, const void* B, float* C, int64_t M, int64_t N, int6
   if (n_tm * n_tn > 0x7fffffffLL) return ATTN_E_SHAPE;
   const GemmInstance* inst = nullptr;
   int n = 0;
-  const GemmInstance* table = dtype == ATTN_BF16 ? gemm_instances_bf16(&n) : gemm_instances_f16(&n);
+  const GemmInstance* table = dtype == ATTN_BF16 ? gemm_instances_bf16(&n)
+                              : dtype == ATTN_F16 ? gemm_instances_f16(&n)
+                                                  : gemm_instances_f32(&n);
   for (int i = 0; i < n; ++i)
     if (table[i].t_m == rep.t_m && table[i].t_n == rep.t_n && table[i].t_k == rep.t_k) inst = &table[i];
   if (!inst) return ATTN_E_NO_INSTANCE;

@@ -30,15 +30,28 @@ struct GemmInstance {
 const GemmInstance* gemm_instances_bf16(int* n);
 const GemmInstance* gemm_instances_f16(int* n);
 
-// Fixed structure of the GEMM kernel family: LDS stages of (A, B) tiles, the
+// Fixed structure of a GEMM kernel family: LDS stages of (A, B) tiles, the
 // wave grid over the workgroup tile, waves per SIMD (the register budget),
 // registers per lane outside the accumulators, and the bytes one wave moves
 // per global->LDS copy (each wave copies the same number of whole blocks of
 // every tile).
-constexpr int kGemmStages = 5, kGemmWavesM = 2, kGemmWavesN = 4, kGemmWavesPerSimd = 2, kGemmVgprFixed = 96,
-              kGemmCopyBlock = 1024;
+struct GemmStructure {
+  int stages, waves_m, waves_n, waves_per_simd, vgpr_fixed, copy_block;
+};
+// 16-bit inputs (16x16x32 atom): 8 waves, two per SIMD, 5 stages.
+constexpr GemmStructure kGemm16 = {5, 2, 4, 2, 96, 1024};
+constexpr int kGemmStages = kGemm16.stages, kGemmWavesM = kGemm16.waves_m, kGemmWavesN = kGemm16.waves_n;
+// fp32 inputs (16x16x4 atom, 32 cycles per product): 4 waves, one per SIMD,
+// 3 stages; halving copy blocks per tile keeps every tile the CU rule reaches
+// feasible at 4-byte elements.
+constexpr GemmStructure kGemm32 = {3, 2, 2, 1, 128, 1024};
+
+// The structure of the family that runs `atom` (by its input size).
+const GemmStructure& gemm_structure(const attn_mfma_atom_t* atom);
 
 int derive_gemm(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, int64_t M, int64_t N, int64_t K,
                 attn_gemm_report_t* rep);
+
+const GemmInstance* gemm_instances_f32(int* n);
 
 }  // namespace attn

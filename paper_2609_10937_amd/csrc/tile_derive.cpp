@@ -204,8 +204,8 @@ int derive_softmax(const attn_hw_desc_t* hw, int64_t rows, int64_t n, int elem_b
   return ATTN_OK;
 }
 
-// The GEMM of Section 4 (its worked example) on the same rules, for the GEMM
-// kernel's fixed structure (gemm_internal.h):
+// The GEMM of Section 4 (its worked example) on the same rules, for the
+// structure of the kernel family that runs the atom (gemm_internal.h):
 //   LDS       square tile t = floor(sqrt(LDS / elem)) (the reading of the
 //             printed formula that reproduces the section's own numbers),
 //             each side aligned down to the atom times the waves along it;
@@ -216,21 +216,27 @@ int derive_softmax(const attn_hw_desc_t* hw, int64_t rows, int64_t n, int elem_b
 //             SIMD: the larger side halves until they fit;
 //   CU count  while the grid is below the CU count the larger side halves,
 //             down to one atom per wave.
-static int64_t gemm_vgpr(const attn_mfma_atom_t* atom, int64_t wave_words, int64_t tm, int64_t tn) {
-  const int64_t wm = tm / kGemmWavesM, wn = tn / kGemmWavesN;
-  const int64_t per_atom = cdiv((int64_t)atom->m * atom->n * atom->acc_bytes, wave_words);
-  return (wm / atom->m) * (wn / atom->n) * per_atom + kGemmVgprFixed;
+const GemmStructure& gemm_structure(const attn_mfma_atom_t* atom) {
+  return atom->in_bytes >= 4 ? kGemm32 : kGemm16;
 }
 
-static int64_t gemm_t_k(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, int64_t tm, int64_t tn) {
+static int64_t gemm_vgpr(const GemmStructure& st, const attn_mfma_atom_t* atom, int64_t wave_words, int64_t tm,
+                         int64_t tn) {
+  const int64_t wm = tm / st.waves_m, wn = tn / st.waves_n;
+  const int64_t per_atom = cdiv((int64_t)atom->m * atom->n * atom->acc_bytes, wave_words);
+  return (wm / atom->m) * (wn / atom->n) * per_atom + st.vgpr_fixed;
+}
+
+static int64_t gemm_t_k(const GemmStructure& st, const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom,
+                        int64_t tm, int64_t tn) {
   const int64_t elem = atom->in_bytes;
-  const int64_t unit = (int64_t)kGemmCopyBlock * kGemmWavesM * kGemmWavesN;
+  const int64_t unit = (int64_t)st.copy_block * st.waves_m * st.waves_n;
   int64_t step = atom->k;
   for (const int64_t side : {tm, tn}) {
     const int64_t need = unit / std::gcd(unit, side * elem);
     step = std::lcm(step, need);
   }
-  return hw->lds_bytes / (kGemmStages * (tm + tn) * elem) / step * step;
+  return hw->lds_bytes / (st.stages * (tm + tn) * elem) / step * step;
 }
 
 int derive_gemm(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, int64_t M, int64_t N, int64_t K,
@@ -241,13 +247,14 @@ int derive_gemm(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, int64_t 
   if (atom->m <= 0 || atom->n <= 0 || atom->k <= 0 || atom->in_bytes <= 0 || atom->acc_bytes <= 0)
     return ATTN_E_ARG;
   if (M < 1 || N < 1 || K < 1) return ATTN_E_SHAPE;
+  const GemmStructure& st = gemm_structure(atom);
   memset(rep, 0, sizeof(*rep));
-  rep->stages = kGemmStages;
-  rep->waves_per_wg = kGemmWavesM * kGemmWavesN;
+  rep->stages = st.stages;
+  rep->waves_per_wg = st.waves_m * st.waves_n;
   rep->lds_budget = hw->lds_bytes;
-  const int64_t budget = hw->vgpr_per_thread / kGemmWavesPerSimd;
+  const int64_t budget = hw->vgpr_per_thread / st.waves_per_simd;
   rep->vgpr_budget = (int32_t)budget;
-  const int64_t am = (int64_t)atom->m * kGemmWavesM, an = (int64_t)atom->n * kGemmWavesN;
+  const int64_t am = (int64_t)atom->m * st.waves_m, an = (int64_t)atom->n * st.waves_n;
   const int64_t wave_words = 4 * (int64_t)hw->wavefront_size;
   const int64_t q = hw->lds_bytes / atom->in_bytes;
   int64_t t = (int64_t)std::sqrt((double)q);  // floor(sqrt(q)), corrected to be exact
@@ -259,7 +266,7 @@ int derive_gemm(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, int64_t 
     set_binding(rep, "LDS");
     return ATTN_E_INFEASIBLE;
   }
-  while (gemm_vgpr(atom, wave_words, tm, tn) > budget) {
+  while (gemm_vgpr(st, atom, wave_words, tm, tn) > budget) {
     if (tm >= tn && tm > am) {
       tm = std::max(am, tm / 2 / am * am);
     } else if (tn > an) {
@@ -275,7 +282,7 @@ int derive_gemm(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, int64_t 
     else tn = std::max(an, tn / 2 / an * an);
     binding = "CU";
   }
-  const int64_t tk = gemm_t_k(hw, atom, tm, tn);
+  const int64_t tk = gemm_t_k(st, hw, atom, tm, tn);
   if (tk < atom->k) {
     set_binding(rep, "LDS");
     return ATTN_E_INFEASIBLE;
@@ -285,11 +292,11 @@ int derive_gemm(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, int64_t 
   rep->t_m = (int32_t)tm;
   rep->t_n = (int32_t)tn;
   rep->t_k = (int32_t)tk;
-  rep->warp_m = (int32_t)(tm / kGemmWavesM);
-  rep->warp_n = (int32_t)(tn / kGemmWavesN);
+  rep->warp_m = (int32_t)(tm / st.waves_m);
+  rep->warp_n = (int32_t)(tn / st.waves_n);
   rep->grid = grid;
-  rep->vgpr_est = (int32_t)gemm_vgpr(atom, wave_words, tm, tn);
-  rep->lds_used = (int64_t)kGemmStages * (tm + tn) * tk * atom->in_bytes;
+  rep->vgpr_est = (int32_t)gemm_vgpr(st, atom, wave_words, tm, tn);
+  rep->lds_used = (int64_t)st.stages * (tm + tn) * tk * atom->in_bytes;
   rep->wg_per_cu = (double)grid / hw->num_cus;
   set_binding(rep, binding);
   return ATTN_OK;

@@ -155,5 +155,13 @@ def make_matrix(rows: int, n: int, dtype: str, seed: int, spread: float = 1.0):
     return round_bits(x, dtype)
 
 
+def make_matrix_f32(rows: int, n: int, seed: int, spread: float = 1.0):
+    """A rows x n float32 matrix of N(0,1) values times `spread`."""
+    x = np.random.Generator(np.random.PCG64(seed)).standard_normal((rows, n), dtype=np.float32)
+    if spread != 1.0:
+        x *= np.float32(spread)
+    return x
+
+
 def workload_inputs(w: Workload):
     return make_qkv(w.B, w.H, w.L, w.d, w.dtype, w.seed, w.k_scale)

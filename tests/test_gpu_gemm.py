@@ -97,3 +97,57 @@ def test_rejects_mismatched_tensors():
         capi.attn_gemm(a, b, c)
     with pytest.raises(capi.AttnError):
         capi.attn_gemm(a, a, c.to(torch.bfloat16))
+
+
+# ------------------------------------------------------------ fp32 (the section's own type)
+
+def _run32(M, N, K, seed, spread=1.0):
+    print(f"case gemm fp32 {M}x{N}x{K} seed {seed}", flush=True)
+    a = inputs.make_matrix_f32(M, K, seed=seed, spread=spread)
+    b = inputs.make_matrix_f32(K, N, seed=seed + 1, spread=spread)
+    tc = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    capi.attn_gemm(torch.from_numpy(a).cuda(), torch.from_numpy(b).cuda(), tc)
+    torch.cuda.synchronize()
+    return a.astype(np.float64), b.astype(np.float64), tc.cpu().numpy().astype(np.float64)
+
+
+def _check32(af, bf, got, what):
+    """fp32 products are rounded too: each element is within (K + 4) u |A||B|
+    of the fp64 product (the inner-product bound gamma_K with slack), and the
+    relative Frobenius error stays at a few fp32 roundings."""
+    ref = G.gemm(af, bf)
+    bound = (af.shape[1] + 4) * U32 * G.gemm(np.abs(af), np.abs(bf)) + 1e-30
+    err = np.abs(got - ref)
+    assert np.all(np.isfinite(got)), f"{what}: non-finite output"
+    bad = err > bound
+    assert not bad.any(), f"{what}: {int(bad.sum())} elements beyond (K+4) u |A||B| (max ratio {float((err / bound).max()):.2f})"
+    rel = np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-300)
+    assert rel < 4 * U32 * np.sqrt(af.shape[1]), f"{what}: relative Frobenius error {rel:.3e}"
+    return rel
+
+
+SHAPES32 = [
+    (4096, 4096, 4096),    # the section's 4096^3: 192 x 192 x 32, 484 tiles
+    (4100, 4100, 1000),    # 192 x 192 x 32 with ragged M, N and K
+    (256, 16384, 1000),    # 96 x 192 x 32
+    (256, 8192, 516),      # 96 x 96 x 64, ragged K
+    (64, 16384, 500),      # 32 x 96 x 96, ragged K
+    (100, 64, 40),         # 32 x 32 x 192: one partial k tile
+    (1, 4, 4),             # smallest admitted problem
+]
+
+
+@pytest.mark.parametrize("M,N,K", SHAPES32)
+def test_gemm_fp32_matches_oracle(M, N, K):
+    af, bf, got = _run32(M, N, K, seed=M * 5 + N * 3 + K)
+    rel = _check32(af, bf, got, f"fp32 {M}x{N}x{K}")
+    print(f"  fp32 {M}x{N}x{K}: relative error {rel:.3e}", flush=True)
+
+
+def test_gemm_fp32_identity_is_exact():
+    """A I = A exactly in fp32 (one nonzero term per sum)."""
+    a = inputs.make_matrix_f32(1000, 1000, seed=9)
+    tc = torch.empty((1000, 1000), dtype=torch.float32, device="cuda")
+    capi.attn_gemm(torch.from_numpy(a).cuda(), torch.eye(1000, dtype=torch.float32, device="cuda"), tc)
+    torch.cuda.synchronize()
+    assert np.array_equal(tc.cpu().numpy(), a)
