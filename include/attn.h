@@ -183,8 +183,11 @@ int attn_fwd_merge(const void* workspace, size_t workspace_bytes, void* O,
 /* Unfused baseline (Section 5.4, Table 3): three kernels on `stream` --
  * S = scale Q K^T written to the workspace in `dtype`, the row softmax of
  * attn_softmax overwriting S with P (masked entries 0), then O = P V.  The
- * workspace holds B*H*L*L elements; size it with attn_unfused_workspace_bytes.
- * L must be a multiple of 8 (ATTN_E_SHAPE otherwise). */
+ * two products run on the GEMM kernel of attn_gemm with the tiles
+ * attn_gemm_derive gives for their shapes (L x L x d and L x d x L), in
+ * fp32, written in `dtype`.  The workspace holds B*H*L*L elements; size it
+ * with attn_unfused_workspace_bytes.  L must be a multiple of 8 and at most
+ * 2^22 (ATTN_E_SHAPE otherwise). */
 int attn_fwd_unfused(const void* Q, const void* K, const void* V, void* O,
                      int B, int H, int L, int d, float scale, int causal, int dtype,
                      void* workspace, size_t workspace_bytes, void* stream);

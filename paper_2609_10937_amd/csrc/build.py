@@ -39,6 +39,8 @@ SOURCES = [
     "gemm_bf16.hip",
     "gemm_f16.hip",
     "gemm_f32.hip",
+    "gemm_unfused_bf16.hip",
+    "gemm_unfused_f16.hip",
 ]
 
 ARCH = "gfx950"

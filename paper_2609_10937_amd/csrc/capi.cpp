@@ -12,6 +12,16 @@
 #include "internal.h"
 
 namespace attn {
+const GemmInstance* gemm_instances_qk_bf16(int* n);
+const GemmInstance* gemm_instances_qk_f16(int* n);
+const GemmInstance* gemm_instances_pv_bf16(int* n);
+const GemmInstance* gemm_instances_pv_f16(int* n);
+const GemmInstance* gemm_instances_qk(int dtype, int* n) {
+  return dtype == ATTN_BF16 ? gemm_instances_qk_bf16(n) : gemm_instances_qk_f16(n);
+}
+const GemmInstance* gemm_instances_pv(int dtype, int* n) {
+  return dtype == ATTN_BF16 ? gemm_instances_pv_bf16(n) : gemm_instances_pv_f16(n);
+}
 const FwdInstance* fwd_instances_bf16_d64(int* n);
 const FwdInstance* fwd_instances_bf16_d128(int* n);
 const FwdInstance* fwd_instances_f16_d64(int* n);
@@ -96,6 +106,16 @@ struct DeviceState {
 
 std::mutex g_mu;
 std::map<int, DeviceState> g_dev;
+
+// The unfused baseline's product instance (qk: S = scale Q K^T, else O = P V)
+// for derived tiles, or null.
+const GemmInstance* find_gemm(int dtype, bool qk, const attn_gemm_report_t& r) {
+  int n = 0;
+  const GemmInstance* t = qk ? gemm_instances_qk(dtype, &n) : gemm_instances_pv(dtype, &n);
+  for (int i = 0; i < n; ++i)
+    if (t[i].t_m == r.t_m && t[i].t_n == r.t_n && t[i].t_k == r.t_k) return &t[i];
+  return nullptr;
+}
 
 const FwdInstance* find_instance(int dtype, int d, int t_kv, int q_blocks, int n_waves) {
   using Fn = const FwdInstance* (*)(int*);
@@ -422,7 +442,7 @@ int attn_fwd_unfused(const void* Q, const void* K, const void* V, void* O, int B
   if (rc != ATTN_OK) return rc;
   rc = check_shape(B, H, L, d, dtype);
   if (rc != ATTN_OK) return rc;
-  if (L % 8) return ATTN_E_SHAPE;  // 16-byte rows of the L x L matrix
+  if (L % 8 || L > (1 << 22)) return ATTN_E_SHAPE;  // 16-byte rows of the L x L matrix; K of the P V product
   rc = check_scale(scale);
   if (rc != ATTN_OK) return rc;
   if (!workspace) return ATTN_E_WORKSPACE;
@@ -434,12 +454,20 @@ int attn_fwd_unfused(const void* Q, const void* K, const void* V, void* O, int B
   attn_hw_desc_t desc;
   rc = device_desc(dev, &desc);
   if (rc != ATTN_OK) return rc;
-  attn_softmax_report_t sm;
-  rc = derive_softmax(&desc, (int64_t)B * H * L, L, 2, &sm);
+  UnfusedPlan u;
+  rc = derive_softmax(&desc, (int64_t)B * H * L, L, 2, &u.sm);
   if (rc != ATTN_OK) return rc;
-  if (sm.resident_tiles != kSoftmaxTiles || sm.waves_per_wg != kSoftmaxWaves) return ATTN_E_NO_INSTANCE;
-  const hipError_t e = launch_unfused(Q, K, V, O, workspace, B * H, L, d, scale, causal != 0, dtype, sm,
-                                      static_cast<hipStream_t>(stream));
+  if (u.sm.resident_tiles != kSoftmaxTiles || u.sm.waves_per_wg != kSoftmaxWaves) return ATTN_E_NO_INSTANCE;
+  const attn_mfma_atom_t atom = {16, 16, 32, 2, 4};
+  rc = derive_gemm(&desc, &atom, L, L, d, &u.qk);
+  if (rc != ATTN_OK) return rc;
+  rc = derive_gemm(&desc, &atom, L, d, L, &u.pv);
+  if (rc != ATTN_OK) return rc;
+  u.qk_inst = find_gemm(dtype, true, u.qk);
+  u.pv_inst = find_gemm(dtype, false, u.pv);
+  if (!u.qk_inst || !u.pv_inst) return ATTN_E_NO_INSTANCE;
+  const hipError_t e =
+      launch_unfused(u, Q, K, V, O, workspace, B * H, L, d, scale, causal != 0, dtype, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? ATTN_OK : ATTN_E_HIP;
 }
 

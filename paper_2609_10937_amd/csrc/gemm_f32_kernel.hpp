@@ -218,7 +218,7 @@ __global__ void __launch_bounds__(256) matmul_f32_kernel(const GemmParams p) {
   for (int mb = 0; mb < NMB; ++mb) {
     const int m = m0 + wm * WTM + 16 * mb + c;
     if (m >= M) continue;
-    float* crow = p.c + (size_t)m * N;
+    float* crow = static_cast<float*>(p.c) + (size_t)m * N;
 #pragma unroll
     for (int nb = 0; nb < NNB; ++nb) {
       const int n = n0 + wn * WTN + 16 * nb + 4 * g;

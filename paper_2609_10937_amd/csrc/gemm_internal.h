@@ -9,13 +9,20 @@
 
 namespace attn {
 
-// C[M][N] (fp32) = A[M][K] B[K][N], all row-major and contiguous.
+// C[M][N] = A[M][K] B[K][N], all row-major and contiguous; C is fp32 (or, in
+// the 16-bit family's OUT16 instances, the input type times alpha).  B may
+// be given transposed, as Bt[N][K] (the BT instances).  `batch` independent
+// products run side by side (grid y), matrix z at a + z sa, b + z sb,
+// c + z sc elements.
 struct GemmParams {
   const void* a;
   const void* b;
-  float* c;
+  void* c;
   int M, N, K;
   int n_tm, n_tn;  // workgroup tiles along M and N
+  int batch = 1;
+  int64_t sa = 0, sb = 0, sc = 0;
+  float alpha = 1.f;
 };
 
 using GemmLaunch = hipError_t (*)(const GemmParams&, hipStream_t);
@@ -29,6 +36,10 @@ struct GemmInstance {
 
 const GemmInstance* gemm_instances_bf16(int* n);
 const GemmInstance* gemm_instances_f16(int* n);
+// The unfused attention baseline's products, in the input type: S = scale
+// Q K^T (K given as Bt) and O = P V.
+const GemmInstance* gemm_instances_qk(int dtype, int* n);
+const GemmInstance* gemm_instances_pv(int dtype, int* n);
 
 // Fixed structure of a GEMM kernel family: LDS stages of (A, B) tiles, the
 // wave grid over the workgroup tile, waves per SIMD (the register budget),

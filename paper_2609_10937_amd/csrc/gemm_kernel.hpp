@@ -70,7 +70,10 @@ __device__ __forceinline__ void barrier_only() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int DT, int TM, int TN, int TK, int ST>
+// BT: B is given as Bt[N][K]; its tile then takes the A tile's layout and
+// reads (16-byte chunks of k along a row of Bt).  OUT16: C is written in the
+// input type, times alpha (the products of the unfused attention baseline).
+template <int DT, int TM, int TN, int TK, int ST, bool BT, bool OUT16>
 __global__ void __launch_bounds__(512) matmul_kernel(const GemmParams p) {
   using M_ = Mfma<DT>;
   using V8 = typename M_::V8;
@@ -80,7 +83,7 @@ __global__ void __launch_bounds__(512) matmul_kernel(const GemmParams p) {
   constexpr int NMB = WTM / 16, NNB = WTN / 16, KS = TK / 32;
   constexpr int KCA = TK / 8, KCB = TN / 8;    // 16-byte chunks per row
   constexpr int RA = TK * 2, RB = TN * 2;      // row bytes
-  constexpr int ATB = TM * RA, BTB = TK * RB, SB = ATB + BTB;
+  constexpr int ATB = TM * RA, BTB = TK * TN * 2, SB = ATB + BTB;
   constexpr int LPA = ATB / (1024 * NW), LPB = BTB / (1024 * NW), LPT = LPA + LPB;
   constexpr bool ABLK = KCA == 4;                  // A tile in fragment blocks
   constexpr int KBA = KCA / 4;                     // A blocks per 16 rows (ABLK)
@@ -90,7 +93,7 @@ __global__ void __launch_bounds__(512) matmul_kernel(const GemmParams p) {
   constexpr int PF = F < 6 ? F : 6;
   static_assert(TM % (16 * WM) == 0 && TN % (16 * WN) == 0 && TK % 32 == 0, "atom alignment");
   static_assert(ATB % (1024 * NW) == 0 && BTB % (1024 * NW) == 0, "whole copy blocks per wave");
-  static_assert((ABLK || (NW * RPA) % 16 == 0) && (NW * RPB) % 16 == 0, "swizzle period");
+  static_assert((ABLK || (NW * RPA) % 16 == 0) && (BT || (NW * RPB) % 16 == 0), "swizzle period");
   static_assert(ST >= 3 && 2 * LPT < 64, "stages and copy counter");
   static_assert(ATB + (TK - 4) * RB + 2 * WTN * WN < 65536, "ds offset range");
 
@@ -120,8 +123,9 @@ __global__ void __launch_bounds__(512) matmul_kernel(const GemmParams p) {
   const int m0 = tm * TM, n0 = tn * TN;
   const int n_k = (K + TK - 1) / TK;
 
-  const char* const Ab = static_cast<const char*>(p.a) + (size_t)m0 * K * 2;
-  const char* const Bb = static_cast<const char*>(p.b) + (size_t)n0 * 2;
+  const size_t z = blockIdx.y;  // product of the batch
+  const char* const Ab = static_cast<const char*>(p.a) + (z * p.sa + (size_t)m0 * K) * 2;
+  const char* const Bb = static_cast<const char*>(p.b) + (z * p.sb + (BT ? (size_t)n0 * K : (size_t)n0)) * 2;
   ATTN_LDS char* const lds = (ATTN_LDS char*)smem;
   const uint32_t lds0 = (uint32_t)(size_t)lds;
 
@@ -133,6 +137,7 @@ __global__ void __launch_bounds__(512) matmul_kernel(const GemmParams p) {
   // that XOR the row's swizzle.  Rows past M and columns past N repeat the
   // last row / column (finite data whose results are never stored); k chunks
   // past K are clamped too and their operands zeroed before use.
+  // A tile rows (and, for BT, Bt tile rows): lane offsets of each block.
   int alc, ar0;
   if constexpr (ABLK) {
     alc = lane >> 4;
@@ -145,6 +150,11 @@ __global__ void __launch_bounds__(512) matmul_kernel(const GemmParams p) {
   uint32_t aoff[LPA];
 #pragma unroll
   for (int i = 0; i < LPA; ++i) aoff[i] = (uint32_t)min(ar0 + i * ASTEP, M - 1 - m0) * (uint32_t)(K * 2);
+  uint32_t btoff[BT ? LPB : 1];
+  if constexpr (BT) {
+#pragma unroll
+    for (int i = 0; i < LPB; ++i) btoff[i] = (uint32_t)min(ar0 + i * ASTEP, N - 1 - n0) * (uint32_t)(K * 2);
+  }
   const int br0 = w * RPB + lane / KCB;
   const int blc = (lane % KCB) ^ gemm_b_swz<KCB>(br0);
   const uint32_t bcol = (uint32_t)min(blc, (N - n0) / 8 - 1) * 16;
@@ -155,9 +165,12 @@ __global__ void __launch_bounds__(512) matmul_kernel(const GemmParams p) {
     const int te = min(tt, n_k - 1);
     const int k0 = te * TK;
     const uint32_t dst = (uint32_t)__builtin_amdgcn_readfirstlane(lds0 + (tt % ST) * SB) + w * 1024;
+    const uint32_t ch = (uint32_t)min(alc, (K - k0) / 8 - 1) * 16;
     if (ci < LPA) {
-      const uint32_t ch = (uint32_t)min(alc, (K - k0) / 8 - 1) * 16;
       copy_to_lds(Ab + (size_t)k0 * 2, aoff[ci] + ch, dst + ci * NW * 1024);
+    } else if constexpr (BT) {
+      const int i = ci - LPA;
+      copy_to_lds(Bb + (size_t)k0 * 2, btoff[i] + ch, dst + ATB + i * NW * 1024);
     } else {
       const int i = ci - LPA;
       const uint32_t row = (uint32_t)min(br0 + i * NW * RPB, K - 1 - k0);
@@ -173,14 +186,28 @@ __global__ void __launch_bounds__(512) matmul_kernel(const GemmParams p) {
   // depend only on the lane, and kk, mb, nb enter the address through
   // disjoint bit fields, so each address is a lane base XOR a fragment
   // constant plus an immediate offset.
-  uint32_t la;
-  if constexpr (ABLK) la = (uint32_t)((wm * WTM / 16) * 1024 + 256 * g + 16 * (c ^ g));
-  else la = (uint32_t)((wm * WTM + c) * RA + 16 * (g ^ gemm_a_swz<KCA>(c)));
+  uint32_t la, lbt;
+  if constexpr (ABLK) {
+    la = (uint32_t)((wm * WTM / 16) * 1024 + 256 * g + 16 * (c ^ g));
+    lbt = (uint32_t)(ATB + (wn * WTN / 16) * 1024 + 256 * g + 16 * (c ^ g));
+  } else {
+    la = (uint32_t)((wm * WTM + c) * RA + 16 * (g ^ gemm_a_swz<KCA>(c)));
+    lbt = (uint32_t)(ATB + (wn * WTN + c) * RA + 16 * (g ^ gemm_a_swz<KCA>(c)));
+  }
   const int rb = 8 * g + (c >> 2);
   const int sb = gemm_b_swz<KCB>(rb);
   const uint32_t lb = (uint32_t)(rb * RB + 16 * ((wn * WTN / 8) ^ ((c >> 1) & 1) ^ sb) + 8 * (c & 1));
   auto load = [&](uint32_t sbase, int f) ATTN_INLINE -> V8 {
     const int kk = f / FPK, q = f % FPK;
+    if (BT && q < NNB) {
+      // B^T(kk, nb) from a Bt tile: rows wn WTN + 16 nb + c, k chunk 4 kk + g.
+      if constexpr (ABLK) {
+        ATTN_LDS const char* base = (ATTN_LDS const char*)(size_t)(sbase + lbt);
+        return __builtin_bit_cast(V8, *(ATTN_LDS const u32x4_t*)(base + q * 1024));
+      }
+      ATTN_LDS const char* base = (ATTN_LDS const char*)(size_t)(sbase + ((lbt - ATB) ^ (uint32_t)(64 * kk)) + ATB);
+      return __builtin_bit_cast(V8, *(ATTN_LDS const u32x4_t*)(base + 16 * q * RA));
+    }
     if (q < NNB) {
       ATTN_LDS const char* base = (ATTN_LDS const char*)(size_t)(sbase + (lb ^ (uint32_t)(32 * q)));
       const i16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((ATTN_LDS i16x4_t*)(base + ATB + 32 * kk * RB));
@@ -265,7 +292,7 @@ __global__ void __launch_bounds__(512) matmul_kernel(const GemmParams p) {
 #pragma unroll
       for (int f = 0; f < F; ++f) {
         if (f % FPK >= NNB) __builtin_amdgcn_sched_group_barrier(0x008, NNB, 0);  // matrix products
-        if (((f + PF) % F) % FPK < NNB) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // DS reads
+        if (!BT && ((f + PF) % F) % FPK < NNB) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // DS reads
         else __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
       // This wave's copies of tile j + 2 complete (those of j + 3 .. j + LEAD
@@ -299,19 +326,31 @@ __global__ void __launch_bounds__(512) matmul_kernel(const GemmParams p) {
   for (int mb = 0; mb < NMB; ++mb) {
     const int m = m0 + wm * WTM + 16 * mb + c;
     if (m >= M) continue;
-    float* crow = p.c + (size_t)m * N;
+    const size_t crow = z * p.sc + (size_t)m * N;
 #pragma unroll
     for (int nb = 0; nb < NNB; ++nb) {
       const int n = n0 + wn * WTN + 16 * nb + 4 * g;
-      if (n < N) *reinterpret_cast<f32x4_t*>(crow + n) = acc[nb][mb];
+      if (n >= N) continue;
+      if constexpr (OUT16) {
+        using S = typename M_::S;
+        const f32x4_t v = acc[nb][mb] * p.alpha;
+        S h4[4] = {(S)v[0], (S)v[1], (S)v[2], (S)v[3]};
+        const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, h4[0]) |
+                            ((uint32_t)__builtin_bit_cast(uint16_t, h4[1]) << 16);
+        const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, h4[2]) |
+                            ((uint32_t)__builtin_bit_cast(uint16_t, h4[3]) << 16);
+        *reinterpret_cast<u32x2_t*>(static_cast<uint16_t*>(p.c) + crow + n) = (u32x2_t){lo, hi};
+      } else {
+        *reinterpret_cast<f32x4_t*>(static_cast<float*>(p.c) + crow + n) = acc[nb][mb];
+      }
     }
   }
 }
 
-template <int DT, int TM, int TN, int TK, int ST>
+template <int DT, int TM, int TN, int TK, int ST, bool BT = false, bool OUT16 = false>
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
   const unsigned grid = (unsigned)p.n_tm * (unsigned)p.n_tn;
-  hipLaunchKernelGGL((matmul_kernel<DT, TM, TN, TK, ST>), dim3(grid), dim3(512), 0, s, p);
+  hipLaunchKernelGGL((matmul_kernel<DT, TM, TN, TK, ST, BT, OUT16>), dim3(grid, (unsigned)p.batch), dim3(512), 0, s, p);
   return hipGetLastError();
 }
 

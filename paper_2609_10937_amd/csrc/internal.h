@@ -41,10 +41,18 @@ const FwdInstance* fwd_instances(int* count);
 
 hipError_t launch_combine(const FwdParams& p, int d, int dtype, hipStream_t s);
 
-// sm: the row-softmax derivation for the (B*H*L) x L score matrix.
-hipError_t launch_unfused(const void* q, const void* k, const void* v, void* o, void* ws,
-                          int BH, int L, int d, float scale, int causal, int dtype,
-                          const attn_softmax_report_t& sm, hipStream_t s);
+// The unfused baseline's three steps: the row-softmax derivation for the
+// (B*H*L) x L score matrix and the GEMM derivations (and compiled instances)
+// of its two products.
+struct GemmInstance;
+struct UnfusedPlan {
+  attn_softmax_report_t sm;
+  attn_gemm_report_t qk, pv;
+  const GemmInstance* qk_inst;
+  const GemmInstance* pv_inst;
+};
+hipError_t launch_unfused(const UnfusedPlan& u, const void* q, const void* k, const void* v, void* o, void* ws,
+                          int BH, int L, int d, float scale, int causal, int dtype, hipStream_t s);
 
 hipError_t launch_mfma_probe(int atom, const void* a, const void* b, float* c, hipStream_t s);
 
