@@ -53,20 +53,27 @@ def upload(bits, dtype):
 
 
 def time_steps(fn, steps, warmup):
-    """Warm up, then time exactly `steps` calls; returns (wall ms/step, event ms/step)."""
+    """Warm up, then time exactly `steps` calls back to back (synchronised before
+    and after, no instrumentation between calls); then the same number of calls
+    again with a HIP event pair around each.  Returns (wall ms per call, event
+    ms per call): the first is the throughput, the second the time each call
+    takes on the stream (events add their own gaps between calls)."""
     import torch
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        fn()
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3 / steps
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
-    t0 = time.perf_counter()
     for i in range(steps):
         starts[i].record()
         fn()
         ends[i].record()
     torch.cuda.synchronize()
-    wall = (time.perf_counter() - t0) * 1e3 / steps
     ev = sum(s.elapsed_time(e) for s, e in zip(starts, ends)) / steps
     return wall, ev
 

@@ -7,10 +7,14 @@
 
 namespace attn {
 
-template <int DT, int D>
+// NS > 0: the split count is a compile-time constant, so each thread's loads
+// (NS reference/sum pairs and NS 16-byte partials) issue together; NS = 0
+// reads it from the parameters.  Same arithmetic in the same order either way.
+template <int DT, int D, int NS>
 __global__ void __launch_bounds__(256) combine_kernel(const FwdParams p) {
   using S = typename Mfma<DT>::S;
   constexpr int QUADS = D / 4;
+  const int n_split = NS > 0 ? NS : p.n_split;
   const int64_t rows = (int64_t)p.BH * p.L;
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= rows * QUADS) return;
@@ -19,10 +23,12 @@ __global__ void __launch_bounds__(256) combine_kernel(const FwdParams p) {
   const int64_t stride = rows;  // rows per split
 
   float m = -INFINITY;
-  for (int s = 0; s < p.n_split; ++s) m = fmaxf(m, p.part_ml[(s * stride + row) * 2]);
+#pragma unroll
+  for (int s = 0; s < n_split; ++s) m = fmaxf(m, p.part_ml[(s * stride + row) * 2]);
   float lt = 0.f;
   f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-  for (int s = 0; s < p.n_split; ++s) {
+#pragma unroll
+  for (int s = 0; s < n_split; ++s) {
     const float ms = p.part_ml[(s * stride + row) * 2];
     const float ls = p.part_ml[(s * stride + row) * 2 + 1];
     const float wgt = (ms == -INFINITY) ? 0.f : exp2_hw(ms - m);
@@ -40,20 +46,30 @@ __global__ void __launch_bounds__(256) combine_kernel(const FwdParams p) {
   *reinterpret_cast<u32x2_t*>(static_cast<uint16_t*>(p.o) + row * D + 4 * d4) = (u32x2_t){lo, hi};
 }
 
+template <int DT, int D>
+static void launch_combine_d(const FwdParams& p, unsigned grid, hipStream_t s) {
+  switch (p.n_split) {
+    case 2: hipLaunchKernelGGL((combine_kernel<DT, D, 2>), dim3(grid), dim3(256), 0, s, p); break;
+    case 4: hipLaunchKernelGGL((combine_kernel<DT, D, 4>), dim3(grid), dim3(256), 0, s, p); break;
+    case 8: hipLaunchKernelGGL((combine_kernel<DT, D, 8>), dim3(grid), dim3(256), 0, s, p); break;
+    case 16: hipLaunchKernelGGL((combine_kernel<DT, D, 16>), dim3(grid), dim3(256), 0, s, p); break;
+    default: hipLaunchKernelGGL((combine_kernel<DT, D, 0>), dim3(grid), dim3(256), 0, s, p); break;
+  }
+}
+
+template <int DT>
+static void launch_combine_t(const FwdParams& p, int d, unsigned grid, hipStream_t s) {
+  if (d == 256) launch_combine_d<DT, 256>(p, grid, s);
+  else if (d == 128) launch_combine_d<DT, 128>(p, grid, s);
+  else if (d == 96) launch_combine_d<DT, 96>(p, grid, s);
+  else launch_combine_d<DT, 64>(p, grid, s);
+}
+
 hipError_t launch_combine(const FwdParams& p, int d, int dtype, hipStream_t s) {
   const int64_t threads = (int64_t)p.BH * p.L * (d / 4);
   const unsigned grid = (unsigned)((threads + 255) / 256);
-  if (dtype == ATTN_BF16) {
-    if (d == 256) hipLaunchKernelGGL((combine_kernel<ATTN_BF16, 256>), dim3(grid), dim3(256), 0, s, p);
-    else if (d == 128) hipLaunchKernelGGL((combine_kernel<ATTN_BF16, 128>), dim3(grid), dim3(256), 0, s, p);
-    else if (d == 96) hipLaunchKernelGGL((combine_kernel<ATTN_BF16, 96>), dim3(grid), dim3(256), 0, s, p);
-    else hipLaunchKernelGGL((combine_kernel<ATTN_BF16, 64>), dim3(grid), dim3(256), 0, s, p);
-  } else {
-    if (d == 256) hipLaunchKernelGGL((combine_kernel<ATTN_F16, 256>), dim3(grid), dim3(256), 0, s, p);
-    else if (d == 128) hipLaunchKernelGGL((combine_kernel<ATTN_F16, 128>), dim3(grid), dim3(256), 0, s, p);
-    else if (d == 96) hipLaunchKernelGGL((combine_kernel<ATTN_F16, 96>), dim3(grid), dim3(256), 0, s, p);
-    else hipLaunchKernelGGL((combine_kernel<ATTN_F16, 64>), dim3(grid), dim3(256), 0, s, p);
-  }
+  if (dtype == ATTN_BF16) launch_combine_t<ATTN_BF16>(p, d, grid, s);
+  else launch_combine_t<ATTN_F16>(p, d, grid, s);
   return hipGetLastError();
 }
 
