@@ -212,6 +212,7 @@ def main():
     ap.add_argument("--no-sweep", action="store_true", help="skip the sequence-length sweep (Table 3)")
     ap.add_argument("--no-d256", action="store_true", help="skip the head-dimension-256 workloads")
     ap.add_argument("--no-d96", action="store_true", help="skip the head-dimension-96 workloads")
+    ap.add_argument("--no-d64", action="store_true", help="skip the head-dimension-64 workloads")
     ap.add_argument("--no-softmax", action="store_true", help="skip the row-softmax operator")
     ap.add_argument("--no-gemm", action="store_true", help="skip the GEMM operator")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -265,7 +266,14 @@ def main():
             capi.attn_fwd_unfused(tq, tk, tv, tu, w.scale, w.causal, ws)
 
         _, u_ev = time_steps(ustep, max(3, args.steps // 2), 2)
-        del ws
+        # Context for the baseline's two products: the same shapes through
+        # torch.mm (hipBLASLt), S and P in bf16 like the baseline's.
+        sq, sk, sv = tq.view(w.L, w.d), tk.view(w.L, w.d), tv.view(w.L, w.d)
+        s_lib = ws[:w.L * w.L * 2].view(torch.bfloat16).view(w.L, w.L)
+        o_lib = torch.empty(w.L, w.d, dtype=torch.bfloat16, device="cuda")
+        _, lib_qk = time_steps(lambda: torch.mm(sq, sk.t(), out=s_lib), max(3, args.steps // 2), 2)
+        _, lib_pv = time_steps(lambda: torch.mm(s_lib, sv, out=o_lib), max(3, args.steps // 2), 2)
+        del ws, s_lib, o_lib
         torch.cuda.empty_cache()
 
     secondary = None
@@ -311,41 +319,27 @@ def main():
             del ts, tos, wsu
             torch.cuda.empty_cache()
 
-    d256 = None
-    if not args.no_d256:
-        d256 = []
-        for w3 in inputs.HEAD_DIM_256:
+    def head_dim_leg(workloads):
+        out = []
+        for w3 in workloads:
             print(f"bench: {w3.name}", file=sys.stderr, flush=True)
             t3 = [upload(x, w3.dtype) for x in inputs.workload_inputs(w3)]
             o3 = torch.empty_like(t3[0])
             n3 = 20 if w3.B * w3.H == 1 else 5
             _, ev3 = time_steps(lambda: capi.attn_fwd(t3[0], t3[1], t3[2], o3, w3.scale, w3.causal), n3, n3)
             p3 = capi.attn_fwd_plan(w3.B, w3.H, w3.L, w3.d, w3.causal, capi.ATTN_BF16)
-            d256.append({"workload": w3.name, "ms": round(ev3, 4),
-                         "tflops": round(flops(w3) / (ev3 * 1e-3) / 1e12, 1),
-                         "pct_peak": round(100 * flops(w3) / (ev3 * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 1),
-                         "tiles": {"t_kv": p3.t_kv, "t_q_wave": p3.t_q_wave, "n_waves": p3.n_waves,
-                                   "n_split": p3.n_split, "grid": p3.grid}})
+            out.append({"workload": w3.name, "ms": round(ev3, 4),
+                        "tflops": round(flops(w3) / (ev3 * 1e-3) / 1e12, 1),
+                        "pct_peak": round(100 * flops(w3) / (ev3 * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 1),
+                        "tiles": {"t_kv": p3.t_kv, "t_q_wave": p3.t_q_wave, "n_waves": p3.n_waves,
+                                  "n_split": p3.n_split, "grid": p3.grid}})
             del t3, o3
             torch.cuda.empty_cache()
+        return out
 
-    d96 = None
-    if not args.no_d96:
-        d96 = []
-        for w3 in inputs.HEAD_DIM_96:
-            print(f"bench: {w3.name}", file=sys.stderr, flush=True)
-            t3 = [upload(x, w3.dtype) for x in inputs.workload_inputs(w3)]
-            o3 = torch.empty_like(t3[0])
-            n3 = 20 if w3.B * w3.H == 1 else 5
-            _, ev3 = time_steps(lambda: capi.attn_fwd(t3[0], t3[1], t3[2], o3, w3.scale, w3.causal), n3, n3)
-            p3 = capi.attn_fwd_plan(w3.B, w3.H, w3.L, w3.d, w3.causal, capi.ATTN_BF16)
-            d96.append({"workload": w3.name, "ms": round(ev3, 4),
-                         "tflops": round(flops(w3) / (ev3 * 1e-3) / 1e12, 1),
-                         "pct_peak": round(100 * flops(w3) / (ev3 * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 1),
-                         "tiles": {"t_kv": p3.t_kv, "t_q_wave": p3.t_q_wave, "n_waves": p3.n_waves,
-                                   "n_split": p3.n_split, "grid": p3.grid}})
-            del t3, o3
-            torch.cuda.empty_cache()
+    d256 = None if args.no_d256 else head_dim_leg(inputs.HEAD_DIM_256)
+    d96 = None if args.no_d96 else head_dim_leg(inputs.HEAD_DIM_96)
+    d64 = None if args.no_d64 else head_dim_leg(inputs.HEAD_DIM_64)
 
     smx = None
     if not args.no_softmax:
@@ -458,12 +452,14 @@ def main():
             "ms": round(u_ev, 4), "tflops": round(fl / (u_ev * 1e-3) / 1e12, 2),
             "speedup_fused_over_unfused": round(u_ev / ev_ms, 3),
             "algorithmic_bytes": unfused_bytes(w),
-            "hbm_rate_tbps": round(unfused_bytes(w) / (u_ev * 1e-3) / 1e12, 3)},
+            "hbm_rate_tbps": round(unfused_bytes(w) / (u_ev * 1e-3) / 1e12, 3),
+            "torch_mm_products_ms": {"qk": round(lib_qk, 4), "pv": round(lib_pv, 4)}},
         "parity": parity,
         "secondary": secondary,
         "l_sweep": sweep,
         "head_dim_256": d256,
         "head_dim_96": d96,
+        "head_dim_64": d64,
         "softmax": smx,
         "gemm": gemm,
         "cpu_baseline": cpu,

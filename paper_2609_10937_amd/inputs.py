@@ -79,6 +79,13 @@ HEAD_DIM_96 = (
 )
 WORKLOADS.update({w.name: w for w in HEAD_DIM_96})
 
+# Head dimension 64 (t_kv = 128, 32 rows per wave): the same two shapes.
+HEAD_DIM_64 = (
+    Workload("single_head_l16384_d64", 1, 1, 16384, 64, "bf16", False, 1.0, 1221),
+    Workload("causal_b4h32_l16384_d64", 4, 32, 16384, 64, "bf16", True, 1.0, 1222),
+)
+WORKLOADS.update({w.name: w for w in HEAD_DIM_64})
+
 
 def softmax_scale(d: int) -> float:
     """1/sqrt(d) evaluated in float32, returned as the Python float of that value."""

@@ -127,6 +127,40 @@ def test_sweep_l32768_sampled_rows():
     assert (of <= vf.max(dim=0).values + slack).all() and (of >= vf.min(dim=0).values - slack).all()
 
 
+@pytest.mark.parametrize("name", [w.name for w in inputs.HEAD_DIM_64 + inputs.HEAD_DIM_96 + inputs.HEAD_DIM_256])
+def test_head_dim_workloads_sampled_rows(name):
+    """The head-dimension workloads the benchmark times, at their full sizes:
+    sampled heads and rows against the oracle, and every row inside the range
+    of V (the running range for causal rows)."""
+    w = inputs.WORKLOADS[name]
+    print(f"case workload {w.name} (sampled)", flush=True)
+    q, k, v = inputs.workload_inputs(w)
+    tq, tk, tv = (_gpu.upload(x, w.dtype) for x in (q, k, v))
+    o = _gpu.fused(tq, tk, tv, w.scale, w.causal)
+    L = w.L
+    rng = np.random.default_rng(w.seed)
+    heads = [(0, 0)] if w.B * w.H == 1 else [(0, 0), (w.B - 1, w.H - 1), (1, w.H // 2)]
+    for b, h in heads:
+        rows = np.unique(np.concatenate([np.arange(0, 24), np.arange(L - 24, L),
+                                         rng.integers(0, L, 64), [255, 256, 257, 8191, 8192]]))
+        got = _gpu.download(o[b, h, torch.from_numpy(rows).to("cuda")], w.dtype)
+        ref = A.attention_head(_f64(q[b, h], w.dtype), _f64(k[b, h], w.dtype), _f64(v[b, h], w.dtype),
+                               w.scale, w.causal, rows=rows)
+        mx, mn = _gpu.assert_close(got, ref, w.dtype, f"{w.name} b{b} h{h}")
+        print(f"  {w.name} b{b} h{h}: max_abs {mx:.3e} mean_abs {mn:.3e} over {rows.size} rows", flush=True)
+    of = o.float()
+    vf = tv.float()
+    assert torch.isfinite(of).all()
+    slack = 2e-2
+    if w.causal:
+        vmax = torch.cummax(vf, dim=2).values
+        vmin = -torch.cummax(-vf, dim=2).values
+    else:
+        vmax = vf.max(dim=2, keepdim=True).values
+        vmin = vf.min(dim=2, keepdim=True).values
+    assert (of <= vmax + slack).all() and (of >= vmin - slack).all()
+
+
 # ------------------------------------------------------------ edge shapes
 
 EDGE = [(L, d, causal, dt) for L in (1, 17, 100, 1000, 4097) for d in (64, 96, 128, 256)
