@@ -138,7 +138,9 @@ int attn_vgpr_estimate(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom,
 
 /* Closed-formula tile derivation (Sections 4 and 5.4): LDS fixes t_kv, the
  * register budget fixes t_q_wave, the CU count bounds the grid (splitting the
- * key range, then shrinking the Q tile), and every tile is atom aligned.
+ * key range into the count with the fewest rounds of num_cus workgroups times
+ * key tiles per split, then shrinking the Q tile if even the most splits leave
+ * CUs idle), and every tile is atom aligned.
  * Returns ATTN_OK with report->feasible = 1, or ATTN_E_INFEASIBLE with
  * report->binding naming the constraint that failed.  Host-only integer math. */
 int attn_tile_derive(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom,

@@ -134,19 +134,29 @@ def derive(hw, atom, op, st):
     n_qt = _cdiv(op.L, n_w * t_q)
     heads = op.B * op.H
     n_split = 1
+    fills = False
     if heads * n_qt < hw.num_cus and st.max_split > 1:
-        need = _cdiv(hw.num_cus, heads * n_qt)
-        want = 1
-        while want < need:
-            want *= 2
-        n_split = min(want, st.max_split, n_kv)
-        n_split = _cdiv(n_kv, _cdiv(n_kv, n_split))   # drop empty splits
+        # Split count (our addition to the CU rule): the grid runs in rounds of
+        # num_cus workgroups and a workgroup's time follows its key tiles, so
+        # take the count with the fewest rounds x tiles per split (the smallest
+        # on ties).  Counts that leave a split empty collapse onto a smaller one.
+        s_max = _cdiv(n_kv, _cdiv(n_kv, min(st.max_split, n_kv)))
+        best = None
+        for s in range(1, s_max + 1):
+            per = _cdiv(n_kv, s)
+            eff = _cdiv(n_kv, per)
+            cost = _cdiv(heads * n_qt * eff, hw.num_cus) * per
+            if best is None or cost < best[0]:
+                best = (cost, eff)
+        fills = heads * n_qt * s_max >= hw.num_cus
+        n_split = best[1] if fills else s_max
         if n_split > 1:
             binding = "CU"
-    # Still fewer workgroups than CUs: shrink the Q tile, first by halving the
-    # waves per workgroup (if the registers that staging needs per lane still
-    # fit), else by one atom step of the per-wave tile.
-    while heads * n_qt * n_split < hw.num_cus:
+    # Fewer workgroups than CUs that splitting cannot make up: shrink the Q
+    # tile, first by halving the waves per workgroup (if the registers that
+    # staging needs per lane still fit), else by one atom step of the per-wave
+    # tile.
+    while not fills and heads * n_qt * n_split < hw.num_cus:
         if n_w > 1 and vgpr_count(hw, atom, op, st, t_q, t_kv, n_w // 2) <= budget:
             n_w //= 2
         elif t_q > align_q:

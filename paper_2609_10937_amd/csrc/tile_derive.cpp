@@ -117,15 +117,25 @@ int derive_tiles(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const a
   const int64_t n_kv = cdiv(op->L, t_kv);
   int64_t n_qt = cdiv(op->L, n_w * t_q);
   int64_t n_split = 1;
+  bool fills = false;
   if (heads * n_qt < hw->num_cus && op->max_split > 1) {
-    const int64_t need = cdiv(hw->num_cus, heads * n_qt);
-    int64_t want = 1;
-    while (want < need) want *= 2;
-    n_split = std::min(std::min(want, (int64_t)op->max_split), n_kv);
-    n_split = cdiv(n_kv, cdiv(n_kv, n_split));  // no empty splits
+    // The grid runs in rounds of num_cus workgroups and a workgroup's time
+    // follows its key tiles: take the split count with the fewest rounds x
+    // tiles per split, the smallest on ties; a count that would leave a split
+    // empty collapses onto the smaller count with the same tiles per split.
+    const int64_t s_max = cdiv(n_kv, cdiv(n_kv, std::min((int64_t)op->max_split, n_kv)));
+    int64_t best_cost = -1, best = 1;
+    for (int64_t s = 1; s <= s_max; ++s) {
+      const int64_t per = cdiv(n_kv, s), eff = cdiv(n_kv, per);
+      const int64_t cost = cdiv(heads * n_qt * eff, hw->num_cus) * per;
+      if (best_cost < 0 || cost < best_cost) best_cost = cost, best = eff;
+    }
+    fills = heads * n_qt * s_max >= hw->num_cus;
+    n_split = fills ? best : s_max;
     if (n_split > 1) binding = "CU";
   }
-  while (heads * n_qt * n_split < hw->num_cus) {
+  // Fewer workgroups than CUs that splitting cannot make up: shrink the Q tile.
+  while (!fills && heads * n_qt * n_split < hw->num_cus) {
     if (n_w > 1 && vgpr_estimate(hw, atom, op, t_q, t_kv, n_w / 2) <= budget)
       n_w /= 2;
     else if (t_q > align_q)

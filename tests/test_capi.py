@@ -164,6 +164,28 @@ def test_headline_plans():
     assert (r.n_split, r.grid, r.binding) == (1, 8192, b"VGPR")
 
 
+@pytest.mark.parametrize("shape,split,grid", [
+    # 64 query tiles, 256 key tiles: 4 splits fill one round exactly (8 tie at
+    # two rounds of 32 tiles; the smaller count wins)
+    ((1, 1, 16384, 128), 4, 256),
+    # d = 96: 43 query tiles of 384 rows, 256 key tiles.  8 splits: 344
+    # workgroups, two rounds of 32 tiles = 64; 5 splits: one round of 52;
+    # 11 splits: two rounds of 24 = 48, the fewest
+    ((1, 1, 16384, 96), 11, 473),
+    # L = 10000: 40 query tiles, 157 key tiles; 6 splits of 27 tiles make one
+    # round of 240 (8 splits: 320 workgroups, two rounds of 20 = 40)
+    ((1, 1, 10000, 128), 6, 240),
+    # splitting cannot fill the CUs: the most splits (16), then halve the waves
+    ((1, 4, 1000, 96), 16, 384),
+])
+def test_split_count_by_rounds(shape, split, grid):
+    """The split count minimises rounds of CU-count workgroups times key tiles
+    per split (worked by hand in each case)."""
+    hw = capi.attn_hw_desc_preset("gfx950")
+    r = capi.attn_fwd_plan(*shape, 0, capi.ATTN_BF16, hw=hw)
+    assert (r.n_split, r.grid, r.binding) == (split, grid, b"CU")
+
+
 # ------------------------------------------------------------ argument checks
 
 P = 1 << 20  # a 16-byte aligned fake device address; never dereferenced
@@ -287,7 +309,10 @@ def test_gfx942_class_descriptor():
     assert (atom.m, atom.n, atom.k) == (16, 16, 16)
     op = capi.attn_fwd_op(1, 1, 16384, 128, 0, capi.ATTN_BF16)
     rc, r = capi.attn_tile_derive(hw, atom, op)
-    assert rc == 0 and r.t_kv == 16 and r.lds_used == 10 * 16 * 128 * 2 and r.grid >= hw.num_cus
+    assert rc == 0 and r.t_kv == 16 and r.lds_used == 10 * 16 * 128 * 2
+    # 43 query tiles of 384 rows, 1024 key tiles: 7 splits of 147 tiles fill
+    # one round of 301 workgroups on 304 CUs (8 splits would take two rounds).
+    assert (r.tile_q, r.n_split, r.grid) == (384, 7, 301)
     assert r.vgpr_est <= r.vgpr_budget == 256
     op = capi.attn_fwd_op(1, 1, 16384, 256, 0, capi.ATTN_BF16)
     rc, r = capi.attn_tile_derive(hw, atom, op)

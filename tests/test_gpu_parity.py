@@ -167,6 +167,22 @@ EDGE = [(L, d, causal, dt) for L in (1, 17, 100, 1000, 4097) for d in (64, 96, 1
         for causal in (False, True) for dt in ("bf16", "f16")]
 
 
+@pytest.mark.parametrize("L,d,causal,dtype", [(10000, 128, False, "bf16"), (10000, 128, True, "f16"),
+                                               (9000, 96, False, "bf16")])
+def test_split_counts_not_powers_of_two(L, d, causal, dtype):
+    """Single heads whose derived key split is not a power of two (the merge
+    then reads its split count at run time): all rows against the oracle."""
+    dt = capi.ATTN_BF16 if dtype == "bf16" else capi.ATTN_F16
+    plan = capi.attn_fwd_plan(1, 1, L, d, causal, dt)
+    assert plan.n_split > 1 and plan.n_split & (plan.n_split - 1)
+    print(f"case split L{L} d{d} causal{int(causal)} {dtype} n_split {plan.n_split}", flush=True)
+    q, k, v = inputs.make_qkv(1, 1, L, d, dtype, seed=L + d)
+    scale = inputs.softmax_scale(d)
+    o = _gpu.fused(_gpu.upload(q, dtype), _gpu.upload(k, dtype), _gpu.upload(v, dtype), scale, causal)
+    ref = A.attention(_f64(q, dtype), _f64(k, dtype), _f64(v, dtype), scale, causal)
+    _gpu.assert_close(_gpu.download(o, dtype), ref, dtype, f"split L{L} d{d}")
+
+
 @pytest.mark.parametrize("L,d,causal,dtype", EDGE)
 def test_edge_shapes(L, d, causal, dtype):
     B, H = (2, 3) if L <= 1000 else (1, 2)

@@ -86,7 +86,9 @@ def test_cu_rule_splits_then_shrinks():
     st = T.Structure(kv_lds_num=1, kv_lds_den=1, kv_tiles=8, stage_tiles=2, waves_per_wg=8,
                      waves_per_simd=2, vgpr_fixed=32, max_split=8)
     rep = T.derive(hw, atom, T.Op(1, 1, 16384, 128, 2), st)
-    assert rep["feasible"] and rep["n_split"] > 1 and rep["grid"] >= 256
+    # 43 query tiles of 384 rows, 256 key tiles, at most 8 splits: 5 splits make
+    # one round of 215 workgroups x 52 tiles, 8 splits two rounds x 32 tiles
+    assert rep["feasible"] and (rep["tile_q"], rep["n_split"], rep["grid"]) == (384, 5, 215)
     assert rep["binding"] == "CU"
     st1 = T.Structure(**{**st.__dict__, "max_split": 1})
     rep1 = T.derive(hw, atom, T.Op(1, 1, 16384, 128, 2), st1)
