@@ -7,14 +7,16 @@
 
 namespace attn {
 
-// NS > 0: the split count is a compile-time constant, so each thread's loads
-// (NS reference/sum pairs and NS 16-byte partials) issue together; NS = 0
-// reads it from the parameters.  Same arithmetic in the same order either way.
+// NS is a compile-time bound on the split count (2, 4, 8 or 16), so each
+// thread's loads (NS reference/sum pairs and NS 16-byte partials) issue
+// together.  Slots past the actual count n re-read split n - 1 (cache hits)
+// and take weight 0, which leaves the maximum, the sum and the accumulator
+// unchanged.
 template <int DT, int D, int NS>
 __global__ void __launch_bounds__(256) combine_kernel(const FwdParams p) {
   using S = typename Mfma<DT>::S;
   constexpr int QUADS = D / 4;
-  const int n_split = NS > 0 ? NS : p.n_split;
+  const int n_split = p.n_split;
   const int64_t rows = (int64_t)p.BH * p.L;
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= rows * QUADS) return;
@@ -24,16 +26,17 @@ __global__ void __launch_bounds__(256) combine_kernel(const FwdParams p) {
 
   float m = -INFINITY;
 #pragma unroll
-  for (int s = 0; s < n_split; ++s) m = fmaxf(m, p.part_ml[(s * stride + row) * 2]);
+  for (int s = 0; s < NS; ++s) m = fmaxf(m, p.part_ml[(min(s, n_split - 1) * stride + row) * 2]);
   float lt = 0.f;
   f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int s = 0; s < n_split; ++s) {
-    const float ms = p.part_ml[(s * stride + row) * 2];
-    const float ls = p.part_ml[(s * stride + row) * 2 + 1];
-    const float wgt = (ms == -INFINITY) ? 0.f : exp2_hw(ms - m);
+  for (int s = 0; s < NS; ++s) {
+    const int64_t sr = min(s, n_split - 1) * stride + row;
+    const float ms = p.part_ml[sr * 2];
+    const float ls = p.part_ml[sr * 2 + 1];
+    const float wgt = (s >= n_split || ms == -INFINITY) ? 0.f : exp2_hw(ms - m);
     lt += wgt * ls;
-    const f32x4_t po = *reinterpret_cast<const f32x4_t*>(p.part_o + (s * stride + row) * D + 4 * d4);
+    const f32x4_t po = *reinterpret_cast<const f32x4_t*>(p.part_o + sr * D + 4 * d4);
     acc += wgt * po;
   }
   const float inv = lt > 0.f ? 1.f / lt : 0.f;
@@ -48,13 +51,10 @@ __global__ void __launch_bounds__(256) combine_kernel(const FwdParams p) {
 
 template <int DT, int D>
 static void launch_combine_d(const FwdParams& p, unsigned grid, hipStream_t s) {
-  switch (p.n_split) {
-    case 2: hipLaunchKernelGGL((combine_kernel<DT, D, 2>), dim3(grid), dim3(256), 0, s, p); break;
-    case 4: hipLaunchKernelGGL((combine_kernel<DT, D, 4>), dim3(grid), dim3(256), 0, s, p); break;
-    case 8: hipLaunchKernelGGL((combine_kernel<DT, D, 8>), dim3(grid), dim3(256), 0, s, p); break;
-    case 16: hipLaunchKernelGGL((combine_kernel<DT, D, 16>), dim3(grid), dim3(256), 0, s, p); break;
-    default: hipLaunchKernelGGL((combine_kernel<DT, D, 0>), dim3(grid), dim3(256), 0, s, p); break;
-  }
+  if (p.n_split <= 2) hipLaunchKernelGGL((combine_kernel<DT, D, 2>), dim3(grid), dim3(256), 0, s, p);
+  else if (p.n_split <= 4) hipLaunchKernelGGL((combine_kernel<DT, D, 4>), dim3(grid), dim3(256), 0, s, p);
+  else if (p.n_split <= 8) hipLaunchKernelGGL((combine_kernel<DT, D, 8>), dim3(grid), dim3(256), 0, s, p);
+  else hipLaunchKernelGGL((combine_kernel<DT, D, 16>), dim3(grid), dim3(256), 0, s, p);
 }
 
 template <int DT>
@@ -66,6 +66,7 @@ static void launch_combine_t(const FwdParams& p, int d, unsigned grid, hipStream
 }
 
 hipError_t launch_combine(const FwdParams& p, int d, int dtype, hipStream_t s) {
+  if (p.n_split < 1 || p.n_split > 16) return hipErrorInvalidValue;  // the largest compiled bound
   const int64_t threads = (int64_t)p.BH * p.L * (d / 4);
   const unsigned grid = (unsigned)((threads + 255) / 256);
   if (dtype == ATTN_BF16) launch_combine_t<ATTN_BF16>(p, d, grid, s);
