@@ -29,6 +29,7 @@ WORKLOAD = "single_head_l16384_d128"
 SECONDARY = "causal_b4h32_l16384_d128"
 METRIC = "fused attention fwd TFLOPS (% bf16 MFMA peak) + HBM bytes vs unfused, L=16384 d=128"
 PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 matrix-core peak
+CLOCK_GHZ = 2.4             # the clock the published peak assumes
 PEAK_F32_MFMA_TFLOPS = 157.3  # MI355X dense fp32 matrix-core peak
 HBM_TBPS = 8.0
 
@@ -74,8 +75,24 @@ def time_steps(fn, steps, warmup):
         fn()
         ends[i].record()
     torch.cuda.synchronize()
-    ev = sum(s.elapsed_time(e) for s, e in zip(starts, ends)) / steps
-    return wall, ev
+    times = sorted(s.elapsed_time(e) for s, e in zip(starts, ends))
+    LAST_EVENT_MS[:] = times
+    return wall, sum(times) / steps
+
+
+LAST_EVENT_MS = []  # the per-call event times of the latest time_steps, sorted
+
+
+def event_stats():
+    t = LAST_EVENT_MS
+    return {"median_ms": round(t[len(t) // 2], 5), "min_ms": round(t[0], 5)}
+
+
+def at_clock(tflops, counters):
+    """Fraction of the dense bf16 peak scaled to the clock the counters measured."""
+    if not counters:
+        return None
+    return round(tflops / (PEAK_BF16_TFLOPS * counters["clock_ghz"] / CLOCK_GHZ), 5)
 
 
 def _time_oracle(A, qh, kh, vh, w, dtype):
@@ -252,6 +269,7 @@ def main():
         capi.attn_fwd_partial(tq, tk, tv, to, w.scale, w.causal, ws)
 
     _, k_ms = time_steps(kstep, args.steps, args.warmup)
+    k_stats = event_stats()
     achieved = fl / (k_ms * 1e-3) / 1e12
     del ws
 
@@ -286,10 +304,12 @@ def main():
         o2 = torch.empty_like(t2[0])
         _, ev2 = time_steps(lambda: capi.attn_fwd(t2[0], t2[1], t2[2], o2, w2.scale, w2.causal), 5, 2)
         p2 = capi.attn_fwd_plan(w2.B, w2.H, w2.L, w2.d, w2.causal, capi.ATTN_BF16)
-        secondary = {"workload": w2.name, "ms": round(ev2, 4),
+        mc2 = measured_mfma(w2.name)
+        secondary = {"workload": w2.name, "ms": round(ev2, 4), **event_stats(),
                      "tflops": round(flops(w2) / (ev2 * 1e-3) / 1e12, 2),
                      "pct_peak": round(100 * flops(w2) / (ev2 * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
-                     "mfma_counters": measured_mfma(w2.name),
+                     "frac_at_counter_clock": at_clock(flops(w2) / (ev2 * 1e-3) / 1e12, mc2),
+                     "mfma_counters": mc2,
                      "tiles": {"t_kv": p2.t_kv, "t_q_wave": p2.t_q_wave, "n_waves": p2.n_waves,
                                "n_split": p2.n_split, "grid": p2.grid}}
         del t2, o2
@@ -443,7 +463,9 @@ def main():
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 5),
                      "traffic": measured_traffic(w.name),
                      "kernel": "fwd_kernel (attn_fwd_partial), HIP events per launch",
-                     "kernel_ms": round(k_ms, 5), "step_event_ms": round(ev_ms, 5),
+                     "kernel_ms": round(k_ms, 5), "kernel_ms_median": k_stats["median_ms"],
+                     "kernel_ms_min": k_stats["min_ms"], "step_event_ms": round(ev_ms, 5),
+                     "frac_at_counter_clock": at_clock(achieved, measured_mfma(w.name)),
                      "mfma_counters": measured_mfma(w.name),
                      "algorithmic_flops_per_launch": fl, "algorithmic_bytes_per_launch": fused_bytes(w)},
         "hbm_bytes": {"fused_algorithmic": fused_bytes(w), "unfused_algorithmic": unfused_bytes(w),
