@@ -327,3 +327,27 @@ def test_unfused_baseline(L, causal):
     mx, mn = _gpu.errors(got, ref)
     print(f"  unfused max_abs {mx:.3e} mean_abs {mn:.3e}", flush=True)
     assert np.all(np.isfinite(got)) and mx <= 6e-2 and mn <= 6e-3
+
+
+def test_unfused_baseline_at_the_timed_size():
+    """The baseline as bench.py times it (B = H = 1, L = 16384, d = 128, bf16):
+    sampled rows against the oracle within the baseline's bound, every row finite."""
+    w = inputs.WORKLOADS["single_head_l16384_d128"]
+    print(f"case unfused {w.name} (sampled)", flush=True)
+    q, k, v = inputs.workload_inputs(w)
+    tq, tk, tv = (_gpu.upload(x, w.dtype) for x in (q, k, v))
+    o = torch.empty_like(tq)
+    ws = torch.empty(capi.attn_unfused_workspace_bytes(w.B, w.H, w.L, capi.ATTN_BF16), dtype=torch.uint8,
+                     device="cuda")
+    capi.attn_fwd_unfused(tq, tk, tv, o, w.scale, w.causal, ws)
+    torch.cuda.synchronize()
+    del ws
+    L = w.L
+    rows = np.unique(np.concatenate([np.arange(0, 16), np.arange(L - 16, L),
+                                     np.random.default_rng(79).integers(0, L, 96)]))
+    got = _gpu.download(o[0, 0, torch.from_numpy(rows).to("cuda")], w.dtype)
+    ref = A.attention_head(_f64(q[0, 0], w.dtype), _f64(k[0, 0], w.dtype), _f64(v[0, 0], w.dtype),
+                           w.scale, False, rows=rows)
+    mx, mn = _gpu.errors(got, ref)
+    print(f"  unfused {w.name}: max_abs {mx:.3e} mean_abs {mn:.3e} over {rows.size} rows", flush=True)
+    assert torch.isfinite(o.float()).all() and mx <= 6e-2 and mn <= 6e-3
