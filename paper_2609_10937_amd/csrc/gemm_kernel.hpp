@@ -322,6 +322,45 @@ __global__ void __launch_bounds__(512) matmul_kernel(const GemmParams p) {
   // Epilogue: lane (g, c) of block (nb, mb) holds C[m][n .. n+3] with
   // m = m0 + wm WTM + 16 mb + c, n = n0 + wn WTN + 16 nb + 4 g; N is a
   // multiple of 8, so n < N puts all four columns in range.
+  if constexpr (OUT16) {
+    // 16-bit C goes through LDS (free once every copy has landed and every
+    // wave is past its last read): the fragments are written as rows of the
+    // tile, padded by 32 bytes so the 16 rows of one fragment store take
+    // disjoint 8-bank spans, then read back 16 bytes per lane along rows, so
+    // each global store writes whole row segments of C instead of 16 rows x
+    // 32 bytes.
+    using S = typename M_::S;
+    constexpr int CRB = TN * 2 + 32;  // LDS bytes per C row
+    static_assert(TM * CRB <= ST * SB, "C tile fits the LDS ring");
+    __syncthreads();
+#pragma unroll
+    for (int mb = 0; mb < NMB; ++mb) {
+      const int r = wm * WTM + 16 * mb + c;
+#pragma unroll
+      for (int nb = 0; nb < NNB; ++nb) {
+        const int col = wn * WTN + 16 * nb + 4 * g;
+        const f32x4_t v = acc[nb][mb] * p.alpha;
+        S h4[4] = {(S)v[0], (S)v[1], (S)v[2], (S)v[3]};
+        const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, h4[0]) |
+                            ((uint32_t)__builtin_bit_cast(uint16_t, h4[1]) << 16);
+        const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, h4[2]) |
+                            ((uint32_t)__builtin_bit_cast(uint16_t, h4[3]) << 16);
+        *(ATTN_LDS u32x2_t*)(lds + r * CRB + col * 2) = (u32x2_t){lo, hi};
+      }
+    }
+    __syncthreads();
+    constexpr int CPR = TN / 8;  // 16-byte chunks per C row
+    constexpr int CHUNKS = TM * CPR;
+#pragma unroll
+    for (int ch = tid; ch < CHUNKS; ch += NW * 64) {
+      const int r = ch / CPR, q = ch - r * CPR;
+      const int m = m0 + r, n = n0 + 8 * q;
+      const u32x4_t v = *(ATTN_LDS const u32x4_t*)(lds + r * CRB + 16 * q);
+      if (m < M && n < N)
+        *reinterpret_cast<u32x4_t*>(static_cast<uint16_t*>(p.c) + z * p.sc + (size_t)m * N + n) = v;
+    }
+    return;
+  }
 #pragma unroll
   for (int mb = 0; mb < NMB; ++mb) {
     const int m = m0 + wm * WTM + 16 * mb + c;
@@ -331,18 +370,7 @@ __global__ void __launch_bounds__(512) matmul_kernel(const GemmParams p) {
     for (int nb = 0; nb < NNB; ++nb) {
       const int n = n0 + wn * WTN + 16 * nb + 4 * g;
       if (n >= N) continue;
-      if constexpr (OUT16) {
-        using S = typename M_::S;
-        const f32x4_t v = acc[nb][mb] * p.alpha;
-        S h4[4] = {(S)v[0], (S)v[1], (S)v[2], (S)v[3]};
-        const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, h4[0]) |
-                            ((uint32_t)__builtin_bit_cast(uint16_t, h4[1]) << 16);
-        const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, h4[2]) |
-                            ((uint32_t)__builtin_bit_cast(uint16_t, h4[3]) << 16);
-        *reinterpret_cast<u32x2_t*>(static_cast<uint16_t*>(p.c) + crow + n) = (u32x2_t){lo, hi};
-      } else {
-        *reinterpret_cast<f32x4_t*>(static_cast<float*>(p.c) + crow + n) = acc[nb][mb];
-      }
+      *reinterpret_cast<f32x4_t*>(static_cast<float*>(p.c) + crow + n) = acc[nb][mb];
     }
   }
 }

@@ -308,7 +308,7 @@ def test_bitwise_deterministic():
 
 # ------------------------------------------------------------ unfused baseline
 
-@pytest.mark.parametrize("L,causal", [(1024, False), (256, True)])
+@pytest.mark.parametrize("L,causal", [(1024, False), (256, True), (1000, False), (520, True)])
 def test_unfused_baseline(L, causal):
     """Scores and probabilities are stored in bf16 between the kernels, so the
     baseline is held to a looser bound than the fused kernel (it is a
