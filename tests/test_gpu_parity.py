@@ -351,3 +351,30 @@ def test_unfused_baseline_at_the_timed_size():
     mx, mn = _gpu.errors(got, ref)
     print(f"  unfused {w.name}: max_abs {mx:.3e} mean_abs {mn:.3e} over {rows.size} rows", flush=True)
     assert torch.isfinite(o.float()).all() and mx <= 6e-2 and mn <= 6e-3
+
+
+def _random_cases(n=24, seed=2609):
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        d = int(rng.choice([64, 96, 128, 256]))
+        L = int(rng.integers(1, 3001))
+        B, H = int(rng.integers(1, 3)), int(rng.integers(1, 4))
+        out.append((B, H, L, d, bool(rng.integers(0, 2)), str(rng.choice(["bf16", "f16"])), float(rng.choice([0.5, 1, 3]))))
+    return out
+
+
+@pytest.mark.parametrize("B,H,L,d,causal,dtype,kx", _random_cases())
+def test_random_shapes(B, H, L, d, causal, dtype, kx):
+    """Seeded random shapes (any L up to 3000, every head dimension, both types,
+    causal or not, K spread 0.5-3): all rows against the oracle, through
+    whatever tile, split count and instance the derivation picks."""
+    dt = capi.ATTN_BF16 if dtype == "bf16" else capi.ATTN_F16
+    plan = capi.attn_fwd_plan(B, H, L, d, causal, dt)
+    print(f"case random B{B} H{H} L{L} d{d} causal{int(causal)} {dtype} kx{kx} "
+          f"tile {plan.t_q_wave}x{plan.n_waves} split {plan.n_split}", flush=True)
+    q, k, v = inputs.make_qkv(B, H, L, d, dtype, seed=L * 31 + d, k_scale=kx)
+    scale = inputs.softmax_scale(d)
+    o = _gpu.fused(_gpu.upload(q, dtype), _gpu.upload(k, dtype), _gpu.upload(v, dtype), scale, causal)
+    ref = A.attention(_f64(q, dtype), _f64(k, dtype), _f64(v, dtype), scale, causal)
+    _gpu.assert_close(_gpu.download(o, dtype), ref, dtype, f"random L{L} d{d}")
