@@ -151,3 +151,27 @@ def test_gemm_fp32_identity_is_exact():
     capi.attn_gemm(torch.from_numpy(a).cuda(), torch.eye(1000, dtype=torch.float32, device="cuda"), tc)
     torch.cuda.synchronize()
     assert np.array_equal(tc.cpu().numpy(), a)
+
+
+def _random_gemm_cases(n=16, seed=4096):
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        dtype = str(rng.choice(["bf16", "f16", "f32"]))
+        step = 4 if dtype == "f32" else 8
+        out.append((int(rng.integers(1, 3001)), step * int(rng.integers(1, 3001 // step + 1)),
+                    step * int(rng.integers(1, 2049 // step + 1)), dtype))
+    return out
+
+
+@pytest.mark.parametrize("M,N,K,dtype", _random_gemm_cases())
+def test_gemm_random_shapes(M, N, K, dtype):
+    """Seeded random shapes (any M; N and K multiples of the 16-byte chunk),
+    every type, through whatever tile the derivation picks: the element-wise
+    summation bound against the oracle."""
+    if dtype == "f32":
+        af, bf, got = _run32(M, N, K, seed=M + N + K)
+        _check32(af, bf, got, f"random fp32 {M}x{N}x{K}")
+    else:
+        af, bf, got = _run(M, N, K, dtype, seed=M + N + K)
+        _check(af, bf, got, f"random {dtype} {M}x{N}x{K}")
