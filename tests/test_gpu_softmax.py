@@ -76,3 +76,27 @@ def test_softmax_rows_sum_to_one_large():
                                     np.random.default_rng(4).integers(0, rows, 48)]))
     ref = SM.softmax_rows(inputs.bits_to_f64(x[idx], "bf16"))
     _check(_gpu.download(ty[torch.from_numpy(idx).cuda()], "bf16"), ref, "bf16", "16384 sampled")
+
+
+def _random_softmax_cases(n=16, seed=512):
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        rows = int(rng.integers(1, 400))
+        cols = int(rng.choice([int(rng.integers(1, 70000)), 8 * int(rng.integers(1, 8000))]))
+        out.append((rows, cols, str(rng.choice(["bf16", "f16"])), float(rng.choice([0.1, 1.0, 3.0]))))
+    return out
+
+
+@pytest.mark.parametrize("rows,n,dtype,spread", _random_softmax_cases())
+def test_softmax_random_shapes(rows, n, dtype, spread):
+    """Seeded random shapes (row lengths with and without the 16-byte path,
+    resident or read twice, split or not): every element against the oracle."""
+    print(f"case softmax random {rows}x{n} {dtype} spread {spread}", flush=True)
+    x = inputs.make_matrix(rows, n, dtype, seed=rows * 7 + n, spread=spread)
+    tx = _gpu.upload(x, dtype)
+    ty = torch.empty_like(tx)
+    capi.attn_softmax(tx, ty)
+    torch.cuda.synchronize()
+    ref = SM.softmax_rows(inputs.bits_to_f64(x, dtype))
+    _check(_gpu.download(ty, dtype), ref, dtype, f"random {rows}x{n}")
