@@ -363,7 +363,7 @@ def main():
 
     smx = None
     if not args.no_softmax:
-        # The row-softmax operator of Section 4.3: the paper's 512 x 512 and the
+        # The row-softmax operator of Section 5.3: the paper's 512 x 512 and the
         # score matrix of one L=16384 head; HBM-bound, so reported against 8 TB/s.
         smx = []
         hwq = capi.attn_hw_desc_query(torch.cuda.current_device())

@@ -3,7 +3,7 @@
  *
  * The library computes O = softmax(scale * Q K^T) V per (batch, head) as two
  * chained matrix-core products with an online softmax between them, so the
- * L x L score matrix never reaches device memory (paper: Section 5, the
+ * L x L score matrix never reaches device memory (paper: Section 6, the
  * attention equation, Algorithm 1 and Figure 2).  Tile sizes come from a
  * closed-formula derivation over a hardware descriptor (Sections 3 and 4,
  * Table 2); nothing is searched or tuned at run time.
@@ -136,7 +136,7 @@ int attn_vgpr_estimate(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom,
                        const attn_op_t* op, int t_q_wave, int t_kv, int n_waves,
                        int32_t* out);
 
-/* Closed-formula tile derivation (Sections 4 and 5.4): LDS fixes t_kv, the
+/* Closed-formula tile derivation (Sections 4 and 6.2): LDS fixes t_kv, the
  * register budget fixes t_q_wave, the CU count bounds the grid (splitting the
  * key range into the count with the fewest rounds of num_cus workgroups times
  * key tiles per split, then shrinking the Q tile if even the most splits leave
@@ -155,7 +155,7 @@ int attn_fwd_plan(const attn_hw_desc_t* hw, int B, int H, int L, int d, int caus
 /* Fused attention forward (Algorithm 1 for every Q tile; Figure 2 mapping).
  * scale: finite, >= 0 (1/sqrt(d) for standard attention).  causal != 0 keeps
  * keys j <= i for query i (top-left aligned).  When the derivation splits the
- * key range, partial results are merged with the Section 4.3 operator in a
+ * key range, partial results are merged with the Section 5.3 operator in a
  * second kernel; the workspace for that is held by the library per device,
  * grown on demand and kept until process exit (calls on one device that
  * overlap in time on different streams must not share it: serialise them). */
@@ -163,7 +163,7 @@ int attn_fwd(const void* Q, const void* K, const void* V, void* O,
              int B, int H, int L, int d, float scale, int causal, int dtype, void* stream);
 
 /* The two halves of attn_fwd, for callers that own the workspace (and for
- * timing the fused kernel on its own).  Split-N (Section 4.3): when the
+ * timing the fused kernel on its own).  Split-N (Section 5.3): when the
  * derivation splits the key range, attn_fwd_partial runs the fused kernel
  * and leaves each split's unnormalised output, reference point and running
  * sum in `workspace` (fp32 [n_split][B*H][L][d] followed by
@@ -182,7 +182,7 @@ int attn_fwd_partial(const void* Q, const void* K, const void* V, void* O,
 int attn_fwd_merge(const void* workspace, size_t workspace_bytes, void* O,
                    int B, int H, int L, int d, float scale, int causal, int dtype, void* stream);
 
-/* Unfused baseline (Section 5.4, Table 3): three kernels on `stream` --
+/* Unfused baseline (Section 6.2, Table 3): three kernels on `stream` --
  * S = scale Q K^T written to the workspace in `dtype`, the row softmax of
  * attn_softmax overwriting S with P (masked entries 0), then O = P V.  The
  * two products run on the GEMM kernel of attn_gemm with the tiles
@@ -195,7 +195,7 @@ int attn_fwd_unfused(const void* Q, const void* K, const void* V, void* O,
                      void* workspace, size_t workspace_bytes, void* stream);
 size_t attn_unfused_workspace_bytes(int B, int H, int L, int dtype);
 
-/* Row softmax, the standalone online softmax of Section 4.3, on the same
+/* Row softmax, the standalone online softmax of Section 5.3, on the same
  * CU-centric derivation.  A tile is one 16-byte load per lane of a wave
  * (wavefront_size * 16 / elem_bytes elements); the register budget (at the
  * kernel's 2 waves per SIMD, less its fixed registers) fixes how many tiles a
@@ -273,9 +273,9 @@ int attn_gemm_derive(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, int
                      attn_gemm_report_t* out);
 
 /* C = A B on the matrix cores: A [M][K] and B [K][N] row-major in `dtype`,
- * C [M][N] row-major fp32, every sum in fp32 (Section 4: the GEMM validated
- * against a double-precision reference).  bf16/f16 inputs run on the 16x16x32
- * atom (products exact in fp32), fp32 inputs (ATTN_F32, the section's own
+ * C [M][N] row-major fp32, every sum in fp32 (Section 5.1 validates the
+ * GEMM against a double-precision reference).  bf16/f16 inputs run on the
+ * 16x16x32 atom (products exact in fp32), fp32 inputs (ATTN_F32, the section's own
  * type) on the 16x16x4 fp32 atom, each with its kernel family's tiles from
  * attn_gemm_derive on the current device's descriptor.
  * Sizes: 1 <= M < 2^31; N and K multiples of 8 (bf16/f16) or 4 (fp32), at

@@ -2,11 +2,11 @@
 
 Test infrastructure only (see the package docstring).
 
-Section 5 defines R = softmax(Q K^T / sqrt(d)) V for Q, K, V in R^{L x d};
+Section 6 defines R = softmax(Q K^T / sqrt(d)) V for Q, K, V in R^{L x d};
 the scale is an explicit argument here (the workloads pass 1/sqrt(d) as a
 float32 value).  Causal masking is not defined in the paper; the reading used
 throughout is top-left aligned: row i keeps keys j <= i, and masked logits are
--inf rather than 0 (Section 4.3 explains why a zero would add a spurious
+-inf rather than 0 (Section 5.3 explains why a zero would add a spurious
 positive weight).  Batches and heads are independent [B, H, L, d] slices.
 
 Row blocks only limit memory: each block computes its full rows exactly

@@ -1,4 +1,4 @@
-"""Row softmax and the online softmax of Section 4.3, as plain float64 code.
+"""Row softmax and the online softmax of Section 5.3, as plain float64 code.
 
 Test infrastructure only: only tests/, the smoke check and the benchmark's CPU
 leg may import this module, and it shares no code with the GPU library.
@@ -7,7 +7,7 @@ leg may import this module, and it shares no code with the GPU library.
 exp(x_ij - max_j x_ij), row by row (optionally causal: column j > row index i
 is masked to -inf, the top-left reading used for attention).
 
-``online_stats`` follows the online algorithm of Section 4.3 over column tiles
+``online_stats`` follows the online algorithm of Section 5.3 over column tiles
 of width t: a running maximum m (from -inf) and a running denominator d (from
 0); for every tile the maximum rises to m_new = max(m, tile max), the old sum
 is corrected by s = exp(m - m_new) and the tile's exponentials are added:
@@ -15,7 +15,7 @@ d <- d s + sum exp(x - m_new).  A tile that extends past the row is padded,
 with -inf by default; the paper notes that padding with 0 instead adds exp(0 - m)
 to the denominator, and ``pad`` lets the tests show that.
 
-``merge`` is the associative operator of Section 4.3 on (m, d) pairs, and
+``merge`` is the associative operator of Section 5.3 on (m, d) pairs, and
 ``softmax_split`` cuts each row into contiguous column ranges, runs the online
 algorithm on each range, folds the partial (m, d) with ``merge`` in a binary
 tree (split-N) and writes exp(x - m) / d.

@@ -1,6 +1,6 @@
 """Closed-formula tile derivation for fused attention (model of the C++ routine).
 
-Test infrastructure only.  Written from Sections 3-5 of the paper, applied in
+Test infrastructure only.  Written from Sections 3, 4 and 6 of the paper, applied in
 the paper's CU-centric order (Section 4):
 
 1. LDS -> KV tile.  The staged K/V tiles must fit the LDS share the kernel
@@ -9,14 +9,14 @@ the paper's CU-centric order (Section 4):
    paper's attention instance gives half of LDS to one streamed t_KV x d tile
    (Table 2: t_KV = 64 at d=128, 128 at d=64 with fp32 elements).
 2. VGPR -> Q tile per wave.  Every array live at the synchronisation point
-   between the two GEMMs is counted (Section 5.2, Table 2 caption): the Q
+   between the two GEMMs is counted (Section 6.2, Table 2 caption): the Q
    operand, the fp32 score tile(s), the fp32 output accumulator and the
    running (m, delta) pair, plus the registers used to stage the next K/V tile
    and a fixed overhead.  t_Q is the largest multiple of the atom width whose count
    fits the per-wave budget (Section 4, "VGPR constraint").  The count
    reproduces all four rows of Table 2 with the paper's fp32 instance.
 3. CU count -> grid.  If fewer workgroups than CUs result, the derivation
-   splits the key range (the merge of Section 4.3 is associative), then
+   splits the key range (the merge of Section 5.3 is associative), then
    reduces the Q tile -- waves per workgroup first, then rows per wave --
    until every CU has a workgroup or the tile is one atom (Section 4,
    "Occupancy constraint").
@@ -180,7 +180,7 @@ def derive(hw, atom, op, st):
 
 @dataclasses.dataclass(frozen=True)
 class SoftmaxStructure:
-    """Fixed properties of the row-softmax kernel family (Section 4.3 operator)."""
+    """Fixed properties of the row-softmax kernel family (Section 5.3 operator)."""
     waves_per_wg: int = 4
     waves_per_simd: int = 2
     vgpr_fixed: int = 48
@@ -195,7 +195,7 @@ def derive_softmax(hw: Hardware, rows: int, n: int, elem_bytes: int, st: Softmax
     lane, kept as a power of two.  CU count: a row is split over 2, 4, ...
     waves of a workgroup (never more waves than the workgroup has, never more
     than one per tile) while the grid has fewer workgroups than CUs; the
-    per-wave running statistics are merged with the Section 4.3 operator.
+    per-wave running statistics are merged with the Section 5.3 operator.
     Returns a dict, or None when not even one tile fits the registers.
     """
     if rows < 1 or n < 1:

@@ -1,6 +1,6 @@
 """Closed-form HBM traffic and flop counts of fused vs unfused attention.
 
-Test infrastructure only.  Section 5 (savings equation) and Section 5.4
+Test infrastructure only.  Section 6 (savings equation) and Section 6.2
 ("HBM traffic"): the fused kernel reads Q, K, V and writes the output once,
 4 L d elem bytes per head; the unfused pipeline also writes the L x L score
 matrix, reads it back, writes the probabilities and reads them back,

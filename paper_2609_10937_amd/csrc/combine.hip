@@ -1,4 +1,4 @@
-// Merge of key-range partial results (Section 4.3, the associative operator
+// Merge of key-range partial results (Section 5.3, the associative operator
 // on (max, sum) extended to the output accumulator, applied across splits).
 // Each split's reference point is stored in the base-2 domain (scale log2 e
 // times a logit), so the weights are plain powers of two.

@@ -4,7 +4,7 @@
 // Each wave owns 16*QB query rows and runs Algorithm 1 over the key/value
 // tiles of its workgroup's range:
 //   GEMM1  S^T = K_t Q^T          (v_mfma_f32_16x16x32_{bf16,f16}, fp32 acc)
-//   mask   causal / past-the-end keys -> -inf (Section 4.3 padding rule)
+//   mask   causal / past-the-end keys -> -inf (Section 5.3 padding rule)
 //   stats  running reference max m and sum delta per query row
 //   GEMM2  O^T = V_t^T P^T        (same atom, fp32 acc)
 // Computing S transposed puts query q on lane%16 in both products: the C
@@ -12,7 +12,7 @@
 // to 16 bits, exactly the B operand of the second product once its k index is
 // permuted (k = 8*(lane/16)+e  <->  key 4*(lane/16)+e or 16+4*(lane/16)+e-4).
 // V^T is read with the same permutation by the transposing LDS read.  So P
-// never leaves registers -- the paper's E_t^T LDS round trip (Section 5.3)
+// never leaves registers -- the paper's E_t^T LDS round trip (Section 6.1)
 // is gone.
 //
 // Fragment layouts (Section 3.1: a hardware fact, checked on the device by
@@ -42,7 +42,7 @@
 // are software-pipelined PF fragments ahead of the products that use them.
 //
 // Softmax bookkeeping keeps a per-row reference max m that is only raised
-// when a score would give a weight above 2^8 (the merge of Section 4.3 holds
+// when a score would give a weight above 2^8 (the merge of Section 5.3 holds
 // for any common reference point, so the result is the same).  Most tiles
 // then need neither row maxima nor rescaling of O.  The row sums come from
 // the second product itself (a block of ones times the packed weights), so
@@ -183,7 +183,7 @@ __device__ __forceinline__ int v_swz(int r) {
 // domain relative to the row's reference point mref (cs = scale log2 e; the
 // product is not pre-scaled through Q, whose rounding to 16 bits would
 // double the error of the scores).  The reference of
-// a row can be any common point for all of its keys (the merge of Section 4.3
+// a row can be any common point for all of its keys (the merge of Section 5.3
 // holds for every choice), so it only moves when a weight would exceed 2^8:
 // each lane checks its own scores against lim (8, or -inf while the row has
 // no reference yet) and only if one passes are the row maxima taken and the

@@ -56,7 +56,7 @@ hipError_t launch_unfused(const UnfusedPlan& u, const void* q, const void* k, co
 
 hipError_t launch_mfma_probe(int atom, const void* a, const void* b, float* c, hipStream_t s);
 
-// Row softmax (Section 4.3).  x, y: [rows, n] contiguous; a wave owns `seg`
+// Row softmax (Section 5.3).  x, y: [rows, n] contiguous; a wave owns `seg`
 // elements of a row and `split` waves share a row.
 struct SoftmaxParams {
   const void* x;

@@ -1,15 +1,15 @@
-// Row softmax with the online algorithm of Section 4.3, as a standalone
+// Row softmax with the online algorithm of Section 5.3, as a standalone
 // operator: Y = softmax(X) along each row of a rows x n matrix.
 //
 // A wave owns one segment of a row (the CU rule splits a row over up to the
 // workgroup's waves; their partial statistics are merged with the operator
-// of Section 4.3 through LDS).  The segment is read in tiles of one 16-byte
+// of Section 5.3 through LDS).  The segment is read in tiles of one 16-byte
 // load per lane (64 lanes x 8 elements): for every tile the lane's running
 // maximum m and denominator d take the correction exp(m - m_new) and the
 // tile's exponentials; the first MAXT tiles stay in registers (packed 16-bit),
 // so a segment of up to MAXT tiles is read from HBM once, and longer ones are
 // read again for the output.  Elements past the segment, or above the
-// diagonal when causal, enter as -inf (the padding rule of Section 4.3).
+// diagonal when causal, enter as -inf (the padding rule of Section 5.3).
 // The 64 lanes' (m, d) pairs and then the segments' are merged with the same
 // operator, and the output pass writes exp(x - m) / d in the input type.
 #include <hip/hip_runtime.h>

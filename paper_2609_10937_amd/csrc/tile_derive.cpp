@@ -1,6 +1,6 @@
 // Closed-formula tile derivation for the fused attention kernel.
 //
-// Sections 3-5 of the paper: tiles follow from three hardware constraints in
+// Sections 3, 4 and 6 of the paper: tiles follow from three hardware constraints in
 // a CU-centric order, checked against the atom shape.
 //   1. LDS fixes the key/value tile: the staged tiles fill the LDS share the
 //      kernel structure gives them (Section 4, LDS constraint).
@@ -8,9 +8,9 @@
 //      live at the synchronisation point between the two products: the Q
 //      operand, the fp32 score tile(s), the fp32 output accumulator and the
 //      running max/sum, plus staging registers and a fixed overhead
-//      (Section 5.4, Table 2 caption; Section 4, VGPR constraint).
+//      (Section 6.2, Table 2 caption; Section 4, VGPR constraint).
 //   3. The CU count bounds the grid from below: split the key range (the
-//      merge of Section 4.3 is associative), then shrink the query tile
+//      merge of Section 5.3 is associative), then shrink the query tile
 //      (Section 4, occupancy constraint).
 //   4. Atom alignment (Section 4).
 // The count in step 2 is affine in t_q up to per-array register rounding, so
@@ -162,7 +162,7 @@ int derive_tiles(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const a
   return ATTN_OK;
 }
 
-// The row softmax (Section 4.3) on the same CU-centric rules:
+// The row softmax (Section 5.3) on the same CU-centric rules:
 //   tile      one 16-byte load per lane: wavefront_size * 16 / elem_bytes elements;
 //   registers the budget at the kernel's waves per SIMD, less its fixed
 //             registers, holds R = (budget - fixed) / (16 / 4) packed tiles per

@@ -1,8 +1,8 @@
-// Unfused attention baseline (Section 5.4, Table 3): the L x L score matrix
+// Unfused attention baseline (Section 6.2, Table 3): the L x L score matrix
 // goes to device memory between three kernels.
 //   GEMM (Q K^T):  S = scale Q K^T, stored in the input type
 //   softmax:       S -> P in place, causal-masked entries 0 (the row-softmax
-//                  operator of Section 4.3, attn_softmax, on its own tiles)
+//                  operator of Section 5.3, attn_softmax, on its own tiles)
 //   GEMM (P V):    O = P V, stored in the input type
 // Both products run on the GEMM kernel with the tiles its derivation gives
 // for their shapes (the worked example of Section 4), one product per head

@@ -8,7 +8,7 @@ every value once, to nearest-even, to the storage type (bfloat16 or float16).
 The GPU path and the oracle both consume exactly these rounded values.
 
 The paper measures single-head, d=128 attention over synthetic shapes
-(Section 5, Tables 2 and 3); the named workloads below keep those shapes and
+(Section 6, Tables 2 and 3); the named workloads below keep those shapes and
 add the batched / causal cases used for parity.
 """
 from __future__ import annotations

@@ -1,4 +1,4 @@
-"""GPU parity of the row-softmax operator (Section 4.3) with the float64 oracle."""
+"""GPU parity of the row-softmax operator (Section 5.3) with the float64 oracle."""
 import numpy as np
 import pytest
 

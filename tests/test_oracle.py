@@ -141,7 +141,67 @@ def test_paper_structured_case():
     assert np.max(np.abs(o - v.mean(axis=0))) <= 1e-12
 
 
-# ---------------------------------------------------------------- Algorithm 1
+# ---------------------------------------------------------------- sampled rows and P
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("block_rows", [1, 3, 512])
+def test_sampled_rows_match_brute_force(causal, block_rows):
+    # attention_head(rows=r) evaluates arbitrary, unsorted rows (the GPU tests
+    # compare sampled rows of large workloads through it): each must equal the
+    # pure-Python evaluation of that row, causal rows seeing keys 0..i only.
+    L, d = 23, 6
+    q, k, v = _rand((L, d), 43), _rand((L, d), 44) * 2, _rand((L, d), 45)
+    ref = np.array(brute.attention_brute([[q.tolist()]], [[k.tolist()]], [[v.tolist()]], 0.6, causal))[0, 0]
+    rng = np.random.default_rng(46)
+    for n in (1, 5, L):
+        r = rng.permutation(L)[:n]
+        got = A.attention_head(q, k, v, 0.6, causal, rows=r, block_rows=block_rows)
+        assert got.shape == (n, d)
+        assert np.max(np.abs(got - ref[r])) <= 1e-12
+    # the last row alone, and the first row alone (causal: exactly V[0])
+    assert np.max(np.abs(A.attention_head(q, k, v, 0.6, causal, rows=[L - 1]) - ref[L - 1:])) <= 1e-12
+    if causal:
+        assert np.array_equal(A.attention_head(q, k, v, 0.6, True, rows=[0])[0], v[0])
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_probabilities_match_brute_force(causal):
+    # The full weight matrix against the pure-Python softmax, with a scale that
+    # is not 1: a missing or doubled scale moves every off-uniform entry.
+    L, d = 17, 5
+    q, k = _rand((L, d), 47), _rand((L, d), 48) * 2
+    ref = np.array(brute.probabilities_brute(q.tolist(), k.tolist(), 0.35, causal))
+    got = A.probabilities_head(q, k, 0.35, causal)
+    assert np.max(np.abs(got - ref)) <= 1e-13
+    wrong = A.probabilities_head(q, k, 0.7, causal)
+    assert np.max(np.abs(wrong - ref)) > 1e-2
+
+
+def test_probabilities_hand_case():
+    # Two keys with logits 0 and scale * 2 = ln 3 give weights 1/4 and 3/4.
+    q = np.array([[1.0]])
+    k = np.array([[0.0], [2.0]])
+    p = A.probabilities_head(q, k, math.log(3.0) / 2.0, False)
+    assert p[0] == pytest.approx([0.25, 0.75], abs=1e-15)
+
+
+# ---------------------------------------------------------------- tile fold
+
+def test_tile_triple_hand_case():
+    # One row, logits (0, ln 2) and a masked key: m = ln 2, weights (1/2, 1, 0),
+    # delta = 3/2, O = 1/2 v0 + v1.
+    s = np.array([[0.0, math.log(2.0), -np.inf]])
+    v = np.array([[2.0, 0.0], [0.0, 4.0], [100.0, 100.0]])
+    m, dl, o = online.tile_triple(s, v)
+    assert m[0] == pytest.approx(math.log(2.0), abs=1e-15)
+    assert dl[0] == pytest.approx(1.5, abs=1e-15)
+    assert o[0] == pytest.approx([1.0, 4.0], abs=1e-15)
+    # a fully masked row is the identity: merging it changes nothing
+    e = online.tile_triple(np.full((1, 3), -np.inf), v)
+    assert e[0][0] == -np.inf and e[1][0] == 0.0 and np.all(e[2] == 0.0)
+    mm = online.merge((m, dl, o), e)
+    assert mm[0][0] == m[0] and mm[1][0] == dl[0] and np.array_equal(mm[2], o)
+
 
 @pytest.mark.parametrize("causal", [False, True])
 @pytest.mark.parametrize("t_q,t_kv", [(16, 16), (48, 64), (32, 160), (7, 5)])
@@ -190,8 +250,8 @@ def test_merge_is_associative():
 
 
 def test_zero_padding_would_corrupt_denominator():
-    # Section 4.3: a padded key with logit 0 instead of -inf adds exp(0 - m) > 0
-    # to the denominator.  Plant that mistake in a copy of the tile update and
+    # Section 5.3: a padded key with logit 0 instead of -inf adds exp(0 - m) > 0
+    # to the denominator.  Plant that mistake in a fold over padded tiles and
     # check it moves the result away from the definition; -inf padding does not.
     L, d, t_kv = 10, 4, 8  # the second key tile has 6 padded slots
     q, k, v = _rand((L, d), 38), _rand((L, d), 39), _rand((L, d), 40)
@@ -201,12 +261,12 @@ def test_zero_padding_would_corrupt_denominator():
     vp = np.vstack([v, np.zeros((pad, d))])
 
     def run(pad_value):
-        m, dl, o = np.full(L, -np.inf), np.zeros(L), np.zeros((L, d))
+        acc = online.identity(L, d)
         for j0 in (0, t_kv):
             s = q @ kp[j0:j0 + t_kv].T
             s[:, max(0, L - j0):] = pad_value
-            m, dl, o = online._tile_update(m, dl, o, s, vp[j0:j0 + t_kv])
-        return o / dl[:, None]
+            acc = online.merge(acc, online.tile_triple(s, vp[j0:j0 + t_kv]))
+        return acc[2] / acc[1][:, None]
 
     assert np.max(np.abs(run(-np.inf) - ref)) <= 1e-12
     assert np.max(np.abs(run(0.0) - ref)) > 1e-3

@@ -1,4 +1,4 @@
-"""Pins of the row-softmax oracle (Section 4.3): definition, online algorithm,
+"""Pins of the row-softmax oracle (Section 5.3): definition, online algorithm,
 merge and the padding rule, against brute force, a library routine and
 closed forms."""
 import math
@@ -90,7 +90,7 @@ def test_merge_is_associative_and_commutative():
 
 
 def test_padding_rule():
-    """Section 4.3: a tail tile padded with 0 adds exp(0 - m) per padded entry to
+    """Section 5.3: a tail tile padded with 0 adds exp(0 - m) per padded entry to
     the denominator; padded with -inf it adds nothing."""
     x = np.abs(_rand((4, 100), 11)) + 1.0    # the row maximum stays above the pad value 0
     t = 64

@@ -1,7 +1,7 @@
 """Pins of the tile-derivation and traffic models against the paper's printed values.
 
 Table 2 (all four rows), the gpu_a / gpu_b portability example of Section 3
-and the HBM traffic figures of Section 5.4 are stored in tests/golden with
+and the HBM traffic figures of Section 6.2 are stored in tests/golden with
 their citations.  The remaining checks are properties any correct derivation
 has: budgets never exceeded, tiles aligned to the atom, maximality (one more
 atom step would break the budget) and monotonicity in the budgets.
