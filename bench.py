@@ -1,14 +1,18 @@
 """Fused attention forward benchmark on one MI355X.
 
-python bench.py [--gpus 1] [--steps K] [--warmup W]
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--prewarm-ms T]
 
 A step is one fused attention forward (all of Algorithm 1 for every query
 tile, plus the split merge when the tile derivation splits the key range)
 over the single-head L=16384, d=128 bf16 workload, with Q, K, V already
-resident in device memory.  Prints one JSON line: throughput in TFLOP/s
-(4 L^2 d algorithmic flops per step), the roofline entry of the fused kernel,
-the unfused three-kernel baseline, HBM byte counts of both, and the CPU
-oracle's throughput on the host cores.
+resident in device memory.  W untimed steps, then untimed steps until T ms of
+sustained work have passed (the GPU clock ramps up under load), then K timed
+steps.  Prints one JSON line: throughput in TFLOP/s (4 L^2 d algorithmic
+flops per step), the roofline entry of the fused kernel, the other four
+workload configurations (each with its own roofline entry; the 8-head one
+also with the unfused baseline), the unfused three-kernel baseline, the
+sequence-length sweep, HBM byte counts, and the CPU oracle's throughput on
+the host cores (float32, float64 beside it).
 """
 from __future__ import annotations
 
@@ -26,7 +30,9 @@ sys.path.insert(0, ROOT)
 from paper_2609_10937_amd import capi, inputs  # noqa: E402
 
 WORKLOAD = "single_head_l16384_d128"
-SECONDARY = "causal_b4h32_l16384_d128"
+# The five workload configurations in order, with the timed calls of each.
+CONFIGS = (("tiny_f16_l128_d64", 200), ("h8_l1024_d128", 100), ("causal_b2h16_l4096_d128_kx3", 40),
+           ("single_head_l16384_d128", 0), ("causal_b4h32_l16384_d128", 8))
 METRIC = "fused attention fwd TFLOPS (% bf16 MFMA peak) + HBM bytes vs unfused, L=16384 d=128"
 PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 matrix-core peak
 CLOCK_GHZ = 2.4             # the clock the published peak assumes
@@ -53,15 +59,37 @@ def upload(bits, dtype):
     return t.view(torch.bfloat16 if dtype == "bf16" else torch.float16)
 
 
-def time_steps(fn, steps, warmup):
-    """Warm up, then time exactly `steps` calls back to back (synchronised before
-    and after, no instrumentation between calls); then the same number of calls
-    again with a HIP event pair around each.  Returns (wall ms per call, event
-    ms per call): the first is the throughput, the second the time each call
-    takes on the stream (events add their own gaps between calls)."""
+def prewarm(fn, min_ms):
+    """Untimed sustained calls until at least min_ms of wall time has passed:
+    the GPU raises its clock over the first milliseconds of sustained work
+    (the first launches after an idle period run 10-30% slower), so the timed
+    region starts at the steady clock.  Returns (calls, ms)."""
+    import torch
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    calls = 0
+    while True:
+        for _ in range(10):
+            fn()
+        calls += 10
+        torch.cuda.synchronize()
+        el = (time.perf_counter() - t0) * 1e3
+        if el >= min_ms:
+            return calls, el
+
+
+def time_steps(fn, steps, warmup, warm_ms=0.0):
+    """Warm up (`warmup` calls, then sustained calls until warm_ms of wall time
+    has passed), then time exactly `steps` calls back to back (synchronised
+    before and after, no instrumentation between calls); then the same number
+    of calls again with a HIP event pair around each.  Returns (wall ms per
+    call, event ms per call): the first is the throughput, the second the time
+    each call takes on the stream (events add their own gaps between calls)."""
     import torch
     for _ in range(warmup):
         fn()
+    if warm_ms > 0:
+        LAST_PREWARM[:] = prewarm(fn, warm_ms)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(steps):
@@ -81,6 +109,7 @@ def time_steps(fn, steps, warmup):
 
 
 LAST_EVENT_MS = []  # the per-call event times of the latest time_steps, sorted
+LAST_PREWARM = [0, 0.0]  # (calls, ms) of the latest time-based pre-warm
 
 
 def event_stats():
@@ -95,42 +124,41 @@ def at_clock(tflops, counters):
     return round(tflops / (PEAK_BF16_TFLOPS * counters["clock_ghz"] / CLOCK_GHZ), 5)
 
 
-def _time_oracle(A, qh, kh, vh, w, dtype):
-    """Rows of one head timed through the oracle in `dtype`; the sample grows
-    until it is several seconds of work (bounded by the full head)."""
-    A.attention_head(qh, kh, vh, w.scale, w.causal, rows=np.arange(256), dtype=dtype)  # untimed warm-up
-    rows = 1024
+def _time_oracle(A, qh, kh, vh, w, dtype, min_s):
+    """The oracle over all rows of one head in `dtype`, repeated until at least
+    min_s seconds of work (one untimed warm-up on a row block first).
+    Returns (passes, seconds)."""
+    A.attention_head(qh, kh, vh, w.scale, w.causal, rows=np.arange(256), dtype=dtype)
+    passes, t0 = 0, time.perf_counter()
     while True:
-        t0 = time.perf_counter()
-        A.attention_head(qh, kh, vh, w.scale, w.causal, rows=np.arange(rows), dtype=dtype)
+        A.attention_head(qh, kh, vh, w.scale, w.causal, dtype=dtype)
+        passes += 1
         dt = time.perf_counter() - t0
-        if dt >= 5.0 or rows >= w.L:
-            return rows, dt
-        rows = int(min(w.L, rows * max(2.0, 10.0 / max(dt, 1e-3))))
-        rows = max(1024, rows - rows % 512)
+        if dt >= min_s:
+            return passes, dt
 
 
 def cpu_baseline(w, q, k, v):
-    """The oracle as it stands (float64) on the host cores over a bounded sample
-    of the same workload: every key, a contiguous block of query rows.  The
-    same code in float32 is timed beside it."""
+    """The oracle as it stands, timed on the host's cores over a bounded sample
+    of the same workload (whole passes over its one head, every query row
+    against every key): float32 (the reported value) and float64 (the parity
+    precision), BLAS held to the cores this process may run on."""
+    from threadpoolctl import threadpool_limits
+
     from oracle import attention as A
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:
-        cores = len(os.sched_getaffinity(0))
+    cores = len(os.sched_getaffinity(0))
     qh = inputs.bits_to_f64(q[0, 0], w.dtype)
     kh = inputs.bits_to_f64(k[0, 0], w.dtype)
     vh = inputs.bits_to_f64(v[0, 0], w.dtype)
-    rows, dt = _time_oracle(A, qh, kh, vh, w, np.float64)
-    rows32, dt32 = _time_oracle(A, qh, kh, vh, w, np.float32)
-    fl, fl32 = 4.0 * rows * w.L * w.d, 4.0 * rows32 * w.L * w.d
-    return {"value": fl / dt / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"float64 oracle, query rows 0..{rows - 1} of {w.L} against all {w.L} keys "
-                      f"(B=1, H=1, d={w.d}), {dt:.2f} s",
-            "fp32": {"value": fl32 / dt32 / 1e12, "unit": "TFLOP/s",
-                     "sample": f"the same oracle in float32, query rows 0..{rows32 - 1}, {dt32:.2f} s"}}
+    with threadpool_limits(cores):
+        n32, dt32 = _time_oracle(A, qh, kh, vh, w, np.float32, 10.0)
+        n64, dt64 = _time_oracle(A, qh, kh, vh, w, np.float64, 5.0)
+    fl = flops(w)
+    return {"value": n32 * fl / dt32 / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"float32 oracle, {n32} passes over all {w.L} query rows x {w.L} keys of the "
+                      f"B=1, H=1, d={w.d} head, {dt32:.2f} s",
+            "fp64": {"value": n64 * fl / dt64 / 1e12, "unit": "TFLOP/s",
+                     "sample": f"the same oracle in float64, {n64} passes, {dt64:.2f} s"}}
 
 
 def kernel_source_hash():
@@ -158,6 +186,32 @@ def measured_traffic(workload):
         return None
     entry = rec.get("workloads", {}).get(workload)
     return None if entry is None else entry.get("hbm_bytes_per_launch")
+
+
+def unfused_source_hash():
+    """Hash of the unfused baseline's sources (its products, row softmax and driver)."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_10937_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.startswith("gemm_") or name in ("softmax.hip", "unfused.hip"):
+            with open(os.path.join(csrc, name), "rb") as f:
+                h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_unfused_bytes(workload):
+    """HBM bytes of one unfused-baseline call (its three kernels) from the
+    committed counter summary, if taken on the current sources (else None)."""
+    try:
+        with open(os.path.join(ROOT, "profiles", "unfused_traffic.json")) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_hash") != unfused_source_hash():
+        return None
+    e = rec.get("workloads", {}).get(workload)
+    return None if e is None else e.get("hbm_bytes_per_call")
 
 
 def measured_mfma(workload):
@@ -220,11 +274,14 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    # Sustained work raises the GPU clock over the first few milliseconds;
-    # 50 steps (about 7 ms of kernel time) bring it to its steady level.
     ap.add_argument("--warmup", type=int, default=50)
+    # Sustained work raises the GPU clock over the first milliseconds; after
+    # the --warmup steps, untimed steps continue for this long before timing.
+    ap.add_argument("--prewarm-ms", type=float, default=300.0)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle timing")
-    ap.add_argument("--no-secondary", action="store_true", help="skip the batched causal workload")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the other four workload configurations (tiny f16, 8 heads, batched causal x2)")
+    ap.add_argument("--configs", default="1,2,3,5", help="which of the other configurations to run (1-5)")
     ap.add_argument("--no-unfused", action="store_true", help="skip the unfused baseline")
     ap.add_argument("--no-sweep", action="store_true", help="skip the sequence-length sweep (Table 3)")
     ap.add_argument("--no-d256", action="store_true", help="skip the head-dimension-256 workloads")
@@ -255,7 +312,9 @@ def main():
 
     print("bench: fused", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
-    wall_ms, ev_ms = time_steps(step, args.steps, args.warmup)
+    wall_ms, ev_ms = time_steps(step, args.steps, args.warmup, args.prewarm_ms)
+    prewarm_info = {"calls": LAST_PREWARM[0], "ms": round(LAST_PREWARM[1], 1),
+                    "note": "untimed steps after the --warmup steps, until the GPU clock is steady"}
     fl = flops(w)
     value = fl / (wall_ms * 1e-3) / 1e12
     parity = sampled_parity(w, q, k, v, to)
@@ -268,7 +327,7 @@ def main():
     def kstep():
         capi.attn_fwd_partial(tq, tk, tv, to, w.scale, w.causal, ws)
 
-    _, k_ms = time_steps(kstep, args.steps, args.warmup)
+    _, k_ms = time_steps(kstep, args.steps, args.warmup, 100.0)
     k_stats = event_stats()
     achieved = fl / (k_ms * 1e-3) / 1e12
     del ws
@@ -294,26 +353,71 @@ def main():
         del ws, s_lib, o_lib
         torch.cuda.empty_cache()
 
-    secondary = None
-    if not args.no_secondary:
-        w2 = inputs.WORKLOADS[SECONDARY]
-        print(f"bench: secondary {w2.name}", file=sys.stderr, flush=True)
-        q2, k2, v2 = inputs.workload_inputs(w2)
-        t2 = [upload(x, w2.dtype) for x in (q2, k2, v2)]
-        del q2, k2, v2
+    def config_leg(w2, n_steps, with_unfused=False):
+        """One workload configuration: the whole forward (attn_fwd) and the fused
+        kernel alone (attn_fwd_partial), HIP events per call, after a pre-warm."""
+        dt2 = capi.ATTN_BF16 if w2.dtype == "bf16" else capi.ATTN_F16
+        t2 = [upload(x, w2.dtype) for x in inputs.workload_inputs(w2)]
         o2 = torch.empty_like(t2[0])
-        _, ev2 = time_steps(lambda: capi.attn_fwd(t2[0], t2[1], t2[2], o2, w2.scale, w2.causal), 5, 2)
-        p2 = capi.attn_fwd_plan(w2.B, w2.H, w2.L, w2.d, w2.causal, capi.ATTN_BF16)
+        _, ev2 = time_steps(lambda: capi.attn_fwd(t2[0], t2[1], t2[2], o2, w2.scale, w2.causal), n_steps, 2, 100.0)
+        st2 = event_stats()
+        nb2 = capi.attn_fwd_workspace_bytes(w2.B, w2.H, w2.L, w2.d, w2.causal, dt2)
+        ws2 = torch.empty(max(nb2, 16), dtype=torch.uint8, device="cuda") if nb2 else None
+        _, kev2 = time_steps(lambda: capi.attn_fwd_partial(t2[0], t2[1], t2[2], o2, w2.scale, w2.causal, ws2),
+                             n_steps, 2, 50.0)
+        kst2 = event_stats()
+        p2 = capi.attn_fwd_plan(w2.B, w2.H, w2.L, w2.d, w2.causal, dt2)
+        fl2 = flops(w2)
         mc2 = measured_mfma(w2.name)
-        secondary = {"workload": w2.name, "ms": round(ev2, 4), **event_stats(),
-                     "tflops": round(flops(w2) / (ev2 * 1e-3) / 1e12, 2),
-                     "pct_peak": round(100 * flops(w2) / (ev2 * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
-                     "frac_at_counter_clock": at_clock(flops(w2) / (ev2 * 1e-3) / 1e12, mc2),
-                     "mfma_counters": mc2,
-                     "tiles": {"t_kv": p2.t_kv, "t_q_wave": p2.t_q_wave, "n_waves": p2.n_waves,
-                               "n_split": p2.n_split, "grid": p2.grid}}
+        ach = fl2 / (kst2["median_ms"] * 1e-3) / 1e12
+        entry = {"workload": w2.name, "B": w2.B, "H": w2.H, "L": w2.L, "d": w2.d, "dtype": w2.dtype,
+                 "causal": w2.causal, "k_scale": w2.k_scale,
+                 "ms": round(st2["median_ms"], 5), "ms_mean": round(ev2, 5), "min_ms": st2["min_ms"],
+                 "tflops": round(fl2 / (st2["median_ms"] * 1e-3) / 1e12, 2),
+                 "pct_peak": round(100 * fl2 / (st2["median_ms"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
+                 "roofline": {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS,
+                              "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 5),
+                              "traffic": measured_traffic(w2.name),
+                              "kernel": "fwd_kernel (attn_fwd_partial), HIP events per launch, median",
+                              "kernel_ms": kst2["median_ms"], "kernel_ms_min": kst2["min_ms"],
+                              "frac_at_counter_clock": at_clock(ach, mc2), "mfma_counters": mc2},
+                 "algorithmic_flops": fl2, "algorithmic_bytes": fused_bytes(w2),
+                 "tiles": {"t_kv": p2.t_kv, "t_q_wave": p2.t_q_wave, "n_waves": p2.n_waves,
+                           "n_split": p2.n_split, "grid": p2.grid, "binding": p2.binding.decode()}}
+        del ws2
+        if with_unfused:
+            wsu = torch.empty(capi.attn_unfused_workspace_bytes(w2.B, w2.H, w2.L, dt2), dtype=torch.uint8,
+                              device="cuda")
+            ou = torch.empty_like(o2)
+            _, uev = time_steps(lambda: capi.attn_fwd_unfused(t2[0], t2[1], t2[2], ou, w2.scale, w2.causal, wsu),
+                                n_steps, 2, 50.0)
+            ust = event_stats()
+            entry["unfused"] = {"ms": round(ust["median_ms"], 5),
+                                "tflops": round(fl2 / (ust["median_ms"] * 1e-3) / 1e12, 2),
+                                "speedup_fused_over_unfused": round(ust["median_ms"] / st2["median_ms"], 3),
+                                "algorithmic_bytes": unfused_bytes(w2),
+                                "bytes_ratio": round(unfused_bytes(w2) / fused_bytes(w2), 3),
+                                "measured_bytes": measured_unfused_bytes(w2.name)}
+            del wsu, ou
         del t2, o2
         torch.cuda.empty_cache()
+        return entry
+
+    configs = None
+    if not args.no_configs:
+        # The five workload configurations; the headline (config 4) is the one
+        # timed above, the others here.
+        configs = []
+        chosen = {int(x) for x in args.configs.split(",") if x.strip()}
+        for i, (name, n_steps) in enumerate(CONFIGS, start=1):
+            if i not in chosen:
+                continue
+            if name == WORKLOAD:
+                configs.append({"config": i, "workload": name, "headline": True})
+                continue
+            print(f"bench: config {i} {name}", file=sys.stderr, flush=True)
+            configs.append({"config": i, **config_leg(inputs.WORKLOADS[name], n_steps,
+                                                      with_unfused=name == "h8_l1024_d128")})
 
     sweep = None
     if not args.no_sweep:
@@ -477,7 +581,8 @@ def main():
             "hbm_rate_tbps": round(unfused_bytes(w) / (u_ev * 1e-3) / 1e12, 3),
             "torch_mm_products_ms": {"qk": round(lib_qk, 4), "pv": round(lib_pv, 4)}},
         "parity": parity,
-        "secondary": secondary,
+        "prewarm": prewarm_info,
+        "configs": configs,
         "l_sweep": sweep,
         "head_dim_256": d256,
         "head_dim_96": d96,

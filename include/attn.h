@@ -152,24 +152,36 @@ int attn_tile_derive(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom,
 int attn_fwd_plan(const attn_hw_desc_t* hw, int B, int H, int L, int d, int causal, int dtype,
                   attn_tile_report_t* report);
 
-/* Fused attention forward (Algorithm 1 for every Q tile; Figure 2 mapping).
- * scale: finite, >= 0 (1/sqrt(d) for standard attention).  causal != 0 keeps
- * keys j <= i for query i (top-left aligned).  When the derivation splits the
- * key range, partial results are merged with the Section 5.3 operator in a
- * second kernel; the workspace for that is held by the library per device,
- * grown on demand and kept until process exit (calls on one device that
- * overlap in time on different streams must not share it: serialise them). */
+/* Fused attention forward (Section 6: the attention equation, Algorithm 1 for
+ * every Q tile, Figure 2's mapping).  scale: finite, >= 0 (1/sqrt(d) for
+ * standard attention).  causal != 0 keeps keys j <= i for query i (top-left
+ * aligned).  When the derivation splits the key range (split-N, Section 5.3),
+ * a second kernel merges the splits' partial results with the Section 5.3
+ * operator.
+ * Ownership and ordering: the call only enqueues work on `stream`; it never
+ * synchronises.  The merge's workspace belongs to the library: one buffer per
+ * (device, stream), so concurrent calls on different streams never share
+ * one and calls on one stream use it in stream order.  A stream's buffer is
+ * allocated (hipMalloc) on its first split call and grown when a larger shape
+ * needs more; an outgrown buffer is kept, not freed, until process exit,
+ * since work already enqueued may still use it.  Growing is refused while
+ * `stream` is capturing (ATTN_E_WORKSPACE): capture after a call of the
+ * same or a larger shape on that stream, or use attn_fwd_partial +
+ * attn_fwd_merge with a caller-owned workspace. */
 int attn_fwd(const void* Q, const void* K, const void* V, void* O,
              int B, int H, int L, int d, float scale, int causal, int dtype, void* stream);
 
 /* The two halves of attn_fwd, for callers that own the workspace (and for
  * timing the fused kernel on its own).  Split-N (Section 5.3): when the
  * derivation splits the key range, attn_fwd_partial runs the fused kernel
- * and leaves each split's unnormalised output, reference point and running
- * sum in `workspace` (fp32 [n_split][B*H][L][d] followed by
- * [n_split][B*H][L][2]; the reference is scale*log2(e) times a logit at or
- * below the row's maximum, -inf for a row that saw no key);
- * attn_fwd_merge folds them with the associative merge and writes O.
+ * and leaves in `workspace`, per split and row, the split's output divided
+ * by its own sum, rounded to the input type like O ([n_split][B*H][L][d],
+ * 16-bit), followed by fp32 pairs ([n_split][B*H][L][2]) of the split's
+ * reference point (scale*log2(e) times a logit at or below the row's
+ * maximum; -inf for a row that saw none of the split's keys) and its sum;
+ * attn_fwd_merge weighs the splits with the associative merge and writes O.
+ * The normalised partials add one rounding to the input type before the
+ * merge: |O - exact| <= 2u max|V| + fp32 terms (u = 2^-9 bf16, 2^-12 f16).
  * Without a split the required workspace is 0 bytes, attn_fwd_partial writes
  * O itself and attn_fwd_merge does nothing.  attn_fwd_workspace_bytes gives
  * the size for the current device; the workspace must be 16-byte aligned
@@ -181,6 +193,7 @@ int attn_fwd_partial(const void* Q, const void* K, const void* V, void* O,
                      void* workspace, size_t workspace_bytes, void* stream);
 int attn_fwd_merge(const void* workspace, size_t workspace_bytes, void* O,
                    int B, int H, int L, int d, float scale, int causal, int dtype, void* stream);
+
 
 /* Unfused baseline (Section 6.2, Table 3): three kernels on `stream` --
  * S = scale Q K^T written to the workspace in `dtype`, the row softmax of

@@ -97,11 +97,21 @@ attn_mfma_atom_t atom_for(int dtype) {
   return a;
 }
 
+// attn_fwd's split workspace: one buffer per (device, stream), so calls
+// on different streams never share one, and calls on one stream use it in
+// stream order.  A buffer that is outgrown is retired, never freed: work
+// enqueued earlier (or a graph captured earlier) may still reference it, and
+// freeing would also synchronise the device.
+struct StreamWorkspace {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+};
+
 struct DeviceState {
   bool have_desc = false;
   attn_hw_desc_t desc{};
-  void* ws = nullptr;  // split partial results for attn_fwd
-  size_t ws_bytes = 0;
+  std::map<hipStream_t, StreamWorkspace> ws;
+  std::vector<void*> retired;
 };
 
 std::mutex g_mu;
@@ -193,14 +203,9 @@ int plan(const attn_hw_desc_t* hw, int B, int H, int L, int d, int causal, int d
   return ATTN_OK;
 }
 
-// Checks, derivation and kernel parameters shared by the forward entry
-// points (no device memory is touched).
-struct Prepared {
-  attn_tile_report_t rep;
-  const FwdInstance* inst;
-  FwdParams p;
-  size_t ws_bytes;  // split workspace the plan needs (0 without a split)
-};
+}  // namespace
+
+namespace attn {
 
 int prepare(const void* Q, const void* K, const void* V, void* O, int B, int H, int L, int d, float scale, int causal,
             int dtype, Prepared* out) {
@@ -232,17 +237,17 @@ int prepare(const void* Q, const void* K, const void* V, void* O, int B, int H, 
   p.causal = causal != 0;
   p.c = scale * 1.4426950408889634f;
   const size_t rows = (size_t)p.n_split * p.BH * L;
-  out->ws_bytes = p.n_split > 1 ? rows * (size_t)d * 4 + rows * 8 : 0;
+  out->ws_bytes = p.n_split > 1 ? rows * (size_t)d * 2 + rows * 8 : 0;
   return ATTN_OK;
 }
 
 void bind_workspace(FwdParams& p, void* ws, int d) {
   const size_t rows = (size_t)p.n_split * p.BH * p.L;
-  p.part_o = static_cast<float*>(ws);
-  p.part_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + rows * (size_t)d * 4);
+  p.part_o = ws;
+  p.part_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + rows * (size_t)d * 2);
 }
 
-}  // namespace
+}  // namespace attn
 
 extern "C" {
 
@@ -369,28 +374,29 @@ int attn_fwd(const void* Q, const void* K, const void* V, void* O, int B, int H,
   int rc = prepare(Q, K, V, O, B, H, L, d, scale, causal, dtype, &pr);
   if (rc != ATTN_OK) return rc;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (pr.ws_bytes > 0) {
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return ATTN_E_HIP;
-    std::lock_guard<std::mutex> lk(g_mu);
-    DeviceState& st = g_dev[dev];
-    if (st.ws_bytes < pr.ws_bytes) {
-      // Every earlier use of the old buffer was enqueued on some stream; wait
-      // for the device before releasing it.
-      if (st.ws) {
-        if (hipDeviceSynchronize() != hipSuccess) return ATTN_E_HIP;
-        (void)hipFree(st.ws);
-        st.ws = nullptr;
-        st.ws_bytes = 0;
-      }
-      if (hipMalloc(&st.ws, pr.ws_bytes) != hipSuccess) return ATTN_E_HIP;
-      st.ws_bytes = pr.ws_bytes;
-    }
-    bind_workspace(pr.p, st.ws, d);
+  if (pr.ws_bytes == 0) return pr.inst->launch(pr.p, (unsigned)pr.rep.grid, s) == hipSuccess ? ATTN_OK : ATTN_E_HIP;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return ATTN_E_HIP;
+  // The lock covers binding the stream's buffer and enqueueing both kernels,
+  // so two host threads on one stream cannot interleave their launches.
+  std::lock_guard<std::mutex> lk(g_mu);
+  DeviceState& st = g_dev[dev];
+  StreamWorkspace& w = st.ws[s];
+  if (w.bytes < pr.ws_bytes) {
+    // Allocating is not stream-ordered: never under capture.
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &cap) != hipSuccess) return ATTN_E_HIP;
+    if (cap != hipStreamCaptureStatusNone) return ATTN_E_WORKSPACE;
+    const size_t grow = w.bytes > pr.ws_bytes / 2 ? 2 * w.bytes : pr.ws_bytes;
+    void* nb = nullptr;
+    if (hipMalloc(&nb, grow) != hipSuccess) return ATTN_E_HIP;
+    if (w.ptr) st.retired.push_back(w.ptr);
+    w.ptr = nb;
+    w.bytes = grow;
   }
+  bind_workspace(pr.p, w.ptr, d);
   if (pr.inst->launch(pr.p, (unsigned)pr.rep.grid, s) != hipSuccess) return ATTN_E_HIP;
-  if (pr.p.n_split > 1 && launch_combine(pr.p, d, dtype, s) != hipSuccess) return ATTN_E_HIP;
-  return ATTN_OK;
+  return launch_combine(pr.p, d, dtype, s) == hipSuccess ? ATTN_OK : ATTN_E_HIP;
 }
 
 int attn_fwd_workspace_bytes(int B, int H, int L, int d, int causal, int dtype, size_t* out) {

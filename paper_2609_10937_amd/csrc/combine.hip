@@ -1,11 +1,21 @@
-// Merge of key-range partial results (Section 5.3, the associative operator
-// on (max, sum) extended to the output accumulator, applied across splits).
-// Each split's reference point is stored in the base-2 domain (scale log2 e
-// times a logit), so the weights are plain powers of two.
-// One thread per (row, 4 consecutive output columns).
+// Merge of key-range partial results (Section 5.3: the associative operator
+// on (max, sum), carried over to the output, applied across the splits).
+// Split s left, per row, its output normalised by its own sum (O_s / l_s, in
+// the input type), its reference point m_s in the base-2 domain (scale log2 e
+// times a logit; -inf for a row that saw none of the split's keys) and its
+// sum l_s in fp32.  Against the largest reference M the split weighs
+// w_s = l_s 2^(m_s - M), and the output is sum_s w_s (O_s / l_s) / sum_s w_s.
+// One thread per (row, 8 consecutive output columns): one 16-byte load per
+// split, one 16-byte store.
 #include "fwd_kernel.hpp"
 
 namespace attn {
+
+template <int DT>
+__device__ __forceinline__ float widen(uint16_t h) {
+  if constexpr (DT == ATTN_BF16) return __builtin_bit_cast(float, (uint32_t)h << 16);
+  else return (float)__builtin_bit_cast(_Float16, h);
+}
 
 // NS is a compile-time bound on the split count (2, 4, 8 or 16), so each
 // thread's loads (NS reference/sum pairs and NS 16-byte partials) issue
@@ -15,38 +25,42 @@ namespace attn {
 template <int DT, int D, int NS>
 __global__ void __launch_bounds__(256) combine_kernel(const FwdParams p) {
   using S = typename Mfma<DT>::S;
-  constexpr int QUADS = D / 4;
+  constexpr int OCTS = D / 8;
   const int n_split = p.n_split;
   const int64_t rows = (int64_t)p.BH * p.L;
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= rows * QUADS) return;
-  const int64_t row = idx / QUADS;
-  const int d4 = (int)(idx - row * QUADS);
+  if (idx >= rows * OCTS) return;
+  const int64_t row = idx / OCTS;
+  const int d8 = (int)(idx - row * OCTS);
   const int64_t stride = rows;  // rows per split
 
   float m = -INFINITY;
 #pragma unroll
   for (int s = 0; s < NS; ++s) m = fmaxf(m, p.part_ml[(min(s, n_split - 1) * stride + row) * 2]);
   float lt = 0.f;
-  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
     const int64_t sr = min(s, n_split - 1) * stride + row;
     const float ms = p.part_ml[sr * 2];
     const float ls = p.part_ml[sr * 2 + 1];
-    const float wgt = (s >= n_split || ms == -INFINITY) ? 0.f : exp2_hw(ms - m);
-    lt += wgt * ls;
-    const f32x4_t po = *reinterpret_cast<const f32x4_t*>(p.part_o + sr * D + 4 * d4);
-    acc += wgt * po;
+    const float wgt = (s >= n_split || ms == -INFINITY) ? 0.f : ls * exp2_hw(ms - m);
+    lt += wgt;
+    const u32x4_t po = *reinterpret_cast<const u32x4_t*>(static_cast<const uint16_t*>(p.part_o) + sr * D + 8 * d8);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      acc[2 * e] += wgt * widen<DT>((uint16_t)(po[e] & 0xffffu));
+      acc[2 * e + 1] += wgt * widen<DT>((uint16_t)(po[e] >> 16));
+    }
   }
   const float inv = lt > 0.f ? 1.f / lt : 0.f;
-  acc *= inv;
-  S h4[4] = {(S)acc[0], (S)acc[1], (S)acc[2], (S)acc[3]};
-  const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, h4[0]) |
-                      ((uint32_t)__builtin_bit_cast(uint16_t, h4[1]) << 16);
-  const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, h4[2]) |
-                      ((uint32_t)__builtin_bit_cast(uint16_t, h4[3]) << 16);
-  *reinterpret_cast<u32x2_t*>(static_cast<uint16_t*>(p.o) + row * D + 4 * d4) = (u32x2_t){lo, hi};
+  uint32_t out[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const S a = (S)(acc[2 * e] * inv), b = (S)(acc[2 * e + 1] * inv);
+    out[e] = (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+  }
+  *reinterpret_cast<u32x4_t*>(static_cast<uint16_t*>(p.o) + row * D + 8 * d8) = (u32x4_t){out[0], out[1], out[2], out[3]};
 }
 
 template <int DT, int D>
@@ -67,10 +81,11 @@ static void launch_combine_t(const FwdParams& p, int d, unsigned grid, hipStream
 
 hipError_t launch_combine(const FwdParams& p, int d, int dtype, hipStream_t s) {
   if (p.n_split < 1 || p.n_split > 16) return hipErrorInvalidValue;  // the largest compiled bound
-  const int64_t threads = (int64_t)p.BH * p.L * (d / 4);
-  const unsigned grid = (unsigned)((threads + 255) / 256);
-  if (dtype == ATTN_BF16) launch_combine_t<ATTN_BF16>(p, d, grid, s);
-  else launch_combine_t<ATTN_F16>(p, d, grid, s);
+  const int64_t threads = (int64_t)p.BH * p.L * (d / 8);
+  const int64_t grid = (threads + 255) / 256;
+  if (grid > 0x7fffffffLL) return hipErrorInvalidValue;
+  if (dtype == ATTN_BF16) launch_combine_t<ATTN_BF16>(p, d, (unsigned)grid, s);
+  else launch_combine_t<ATTN_F16>(p, d, (unsigned)grid, s);
   return hipGetLastError();
 }
 

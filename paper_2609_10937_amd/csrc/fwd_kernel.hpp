@@ -659,35 +659,38 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   }
 
   // Epilogue.  Each of the four lane groups holds a partial row sum over its
-  // key subset (same reference), so the total is their sum.  A split leaves
-  // its reference (base 2, -inf for a row that saw no key) beside the sum.
+  // key subset (same reference), so the total is their sum.  Without a split
+  // O / sum is rounded to the input type and stored.  A split stores the same
+  // normalised output of its key range (a convex combination of V rows, so in
+  // the range of the input type), and beside it, in fp32, its reference (base
+  // 2, -inf for a row that saw no key) and its sum, which the merge needs to
+  // weigh the splits.
+  auto store_row = [&](uint16_t* row, const f32x4_t (&acc)[NDB], float inv) ATTN_INLINE {
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      const f32x4_t v = acc[db] * inv;
+      S h4[4] = {(S)v[0], (S)v[1], (S)v[2], (S)v[3]};
+      const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, h4[0]) |
+                          ((uint32_t)__builtin_bit_cast(uint16_t, h4[1]) << 16);
+      const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, h4[2]) |
+                          ((uint32_t)__builtin_bit_cast(uint16_t, h4[3]) << 16);
+      *reinterpret_cast<u32x2_t*>(row + 16 * db + 4 * g) = (u32x2_t){lo, hi};
+    }
+  };
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const float lt = lacc[qb][0];
+    const float inv = lt > 0.f ? 1.f / lt : 0.f;
     int q = q0 + 16 * qb + c;
     // Row offsets at a d that is not a power of two are multiplications: keep
     // the compiler from carrying the Q loads' ones through the loop.
     if constexpr (D != DL) asm volatile("" : "+v"(q));
+    if (q >= L) continue;
     if (p.n_split == 1) {
-      const float inv = lt > 0.f ? 1.f / lt : 0.f;
-      if (q < L) {
-        uint16_t* orow = static_cast<uint16_t*>(p.o) + hoff + (size_t)q * D;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-          const f32x4_t v = o[qb][db] * inv;
-          S h4[4] = {(S)v[0], (S)v[1], (S)v[2], (S)v[3]};
-          const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, h4[0]) |
-                              ((uint32_t)__builtin_bit_cast(uint16_t, h4[1]) << 16);
-          const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, h4[2]) |
-                              ((uint32_t)__builtin_bit_cast(uint16_t, h4[3]) << 16);
-          *reinterpret_cast<u32x2_t*>(orow + 16 * db + 4 * g) = (u32x2_t){lo, hi};
-        }
-      }
-    } else if (q < L) {
+      store_row(static_cast<uint16_t*>(p.o) + hoff + (size_t)q * D, o[qb], inv);
+    } else {
       const size_t prow = ((size_t)split * p.BH + head) * (size_t)L + q;
-      float* po = p.part_o + prow * D;
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) *reinterpret_cast<f32x4_t*>(po + 16 * db + 4 * g) = o[qb][db];
+      store_row(static_cast<uint16_t*>(p.part_o) + prow * D, o[qb], inv);
       if (g == 0)
         *reinterpret_cast<float2*>(p.part_ml + prow * 2) = make_float2(lim[qb] == -INFINITY ? -INFINITY : mref[qb], lt);
     }

@@ -14,8 +14,8 @@ struct FwdParams {
   const void* k;
   const void* v;
   void* o;
-  float* part_o;    // [n_split, BH, L, d] unnormalised partial outputs (n_split > 1)
-  float* part_ml;   // [n_split, BH, L, 2] reference point (base 2) and sum
+  void* part_o;     // [n_split, BH, L, d] per-split outputs normalised by their sums, input type (n_split > 1)
+  float* part_ml;   // [n_split, BH, L, 2] per-split reference point (base 2) and sum
   int BH;
   int L;
   int n_qt;             // query tiles per head
@@ -38,6 +38,20 @@ struct FwdInstance {
 };
 
 const FwdInstance* fwd_instances(int* count);
+
+// Argument checks, tile derivation on the current device's descriptor,
+// instance lookup and kernel parameters shared by the forward entry points
+// (no device memory is touched; the workspace pointers stay unset).
+struct Prepared {
+  attn_tile_report_t rep;
+  const FwdInstance* inst;
+  FwdParams p;
+  size_t ws_bytes;  // split workspace the plan needs (0 without a split)
+};
+int prepare(const void* Q, const void* K, const void* V, void* O, int B, int H, int L, int d, float scale, int causal,
+            int dtype, Prepared* out);
+// Point the split partials of `p` into a workspace of at least Prepared::ws_bytes.
+void bind_workspace(FwdParams& p, void* ws, int d);
 
 hipError_t launch_combine(const FwdParams& p, int d, int dtype, hipStream_t s);
 

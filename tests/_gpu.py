@@ -41,3 +41,23 @@ def assert_close(got, ref, dtype, what=""):
     tmax, tmean = TOL[dtype]
     assert mx <= tmax and mn <= tmean, f"{what}: max_abs {mx:.3e} (<= {tmax}), mean_abs {mn:.3e} (<= {tmean})"
     return mx, mn
+
+
+def oracle_heads_parallel(q64_of, k64_of, v64_of, heads, scale, causal, consume, workers=16):
+    """Evaluate the float64 oracle for each (b, h) in `heads` on a pool of
+    threads (numpy and BLAS release the GIL; BLAS itself is held to one thread
+    per worker) and hand each head's result to consume(b, h, ref) as it
+    completes.  q64_of(b, h) etc. return one head's inputs as float64."""
+    import concurrent.futures as cf
+
+    from threadpoolctl import threadpool_limits
+
+    from oracle import attention as A
+
+    def one(bh):
+        b, h = bh
+        return b, h, A.attention_head(q64_of(b, h), k64_of(b, h), v64_of(b, h), scale, causal, block_rows=256)
+
+    with threadpool_limits(1), cf.ThreadPoolExecutor(workers) as ex:
+        for b, h, ref in ex.map(one, heads):
+            consume(b, h, ref)

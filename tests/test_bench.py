@@ -37,6 +37,23 @@ def test_event_stats_and_clock_scaling():
     assert bench.at_clock(1000.0, None) is None
 
 
+def test_configs_cover_the_five_workloads_in_order():
+    names = [n for n, _ in bench.CONFIGS]
+    assert names == ["tiny_f16_l128_d64", "h8_l1024_d128", "causal_b2h16_l4096_d128_kx3",
+                     "single_head_l16384_d128", "causal_b4h32_l16384_d128"]
+    assert bench.WORKLOAD == names[3]
+    assert all(n > 0 for name, n in bench.CONFIGS if name != bench.WORKLOAD)
+
+
+def test_prewarm_runs_until_the_time_has_passed(monkeypatch):
+    import time
+    torch = pytest.importorskip("torch")
+    monkeypatch.setattr(torch.cuda, "synchronize", lambda: None)
+    calls = []
+    calls_n, ms = bench.prewarm(lambda: (calls.append(1), time.sleep(0.0005)), 20.0)
+    assert ms >= 20.0 and calls_n == len(calls) and calls_n % 10 == 0
+
+
 def test_more_than_one_gpu_is_refused():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
                        text=True, timeout=120)
