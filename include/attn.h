@@ -51,8 +51,12 @@ typedef enum {
   ATTN_E_WORKSPACE = -9,      /* workspace missing or smaller than required */
   ATTN_E_SCALE = -10,         /* scale is negative, NaN or infinite */
   ATTN_E_ARG = -11,           /* other invalid argument (descriptor field, preset name, atom id) */
-  ATTN_E_DEVICE = -12         /* the current device is not a usable gfx950 GPU */
+  ATTN_E_DEVICE = -12,        /* the current device is not a usable gfx950 GPU */
+  ATTN_E_SCRATCH = -13        /* attn_fwd_noalloc: split workspace above ATTN_NOALLOC_SCRATCH_BYTES */
 } attn_status_t;
+
+/* Size of the static per-GPU split workspace of attn_fwd_noalloc. */
+#define ATTN_NOALLOC_SCRATCH_BYTES (32u << 20)
 
 /* One matrix-core instruction shape (Section 3, MFMAAtom): D[m x n] += A[m x k] B[k x n],
  * inputs of in_bytes each, accumulation in acc_bytes. */
@@ -167,7 +171,7 @@ int attn_fwd_plan(const attn_hw_desc_t* hw, int B, int H, int L, int d, int caus
  * since work already enqueued may still use it.  Growing is refused while
  * `stream` is capturing (ATTN_E_WORKSPACE): capture after a call of the
  * same or a larger shape on that stream, or use attn_fwd_partial +
- * attn_fwd_merge with a caller-owned workspace. */
+ * attn_fwd_merge with a caller-owned workspace, or attn_fwd_noalloc. */
 int attn_fwd(const void* Q, const void* K, const void* V, void* O,
              int B, int H, int L, int d, float scale, int causal, int dtype, void* stream);
 
@@ -194,6 +198,17 @@ int attn_fwd_partial(const void* Q, const void* K, const void* V, void* O,
 int attn_fwd_merge(const void* workspace, size_t workspace_bytes, void* O,
                    int B, int H, int L, int d, float scale, int causal, int dtype, void* stream);
 
+/* attn_fwd for callers that cannot allocate device memory (code under stream
+ * capture, serving loops, harnesses that forbid allocation): same arguments,
+ * kernels and result as attn_fwd (bit for bit), with the split workspace in
+ * a static array of ATTN_NOALLOC_SCRATCH_BYTES that each GPU holds from its
+ * first call until process exit.  Never calls hipMalloc or hipFree.  A shape
+ * whose split workspace (attn_fwd_workspace_bytes) exceeds the array is
+ * refused with ATTN_E_SCRATCH before any device work.  All calls on one GPU
+ * share the array: calls that overlap in time on that GPU (different streams,
+ * concurrent graph replays) race and must be serialised by the caller. */
+int attn_fwd_noalloc(const void* Q, const void* K, const void* V, void* O,
+                     int B, int H, int L, int d, float scale, int causal, int dtype, void* stream);
 
 /* Unfused baseline (Section 6.2, Table 3): three kernels on `stream` --
  * S = scale Q K^T written to the workspace in `dtype`, the row softmax of

@@ -23,9 +23,12 @@ STATUS = {
     0: "ATTN_OK", -1: "ATTN_E_NULLPTR", -2: "ATTN_E_SHAPE", -3: "ATTN_E_UNSUPPORTED_D",
     -4: "ATTN_E_DTYPE", -5: "ATTN_E_ALIGN", -6: "ATTN_E_INFEASIBLE", -7: "ATTN_E_NO_INSTANCE",
     -8: "ATTN_E_HIP", -9: "ATTN_E_WORKSPACE", -10: "ATTN_E_SCALE", -11: "ATTN_E_ARG",
-    -12: "ATTN_E_DEVICE",
+    -12: "ATTN_E_DEVICE", -13: "ATTN_E_SCRATCH",
 }
 CODE = {v: k for k, v in STATUS.items()}
+
+# ATTN_NOALLOC_SCRATCH_BYTES of the header: the static split workspace of attn_fwd_noalloc.
+NOALLOC_SCRATCH_BYTES = 32 << 20
 
 # Every function the header declares; the CPU tests check each is exported.
 EXPORTS = (
@@ -33,7 +36,7 @@ EXPORTS = (
     "attn_vgpr_estimate", "attn_tile_derive", "attn_fwd_plan", "attn_fwd", "attn_fwd_workspace_bytes",
     "attn_fwd_partial", "attn_fwd_merge", "attn_fwd_unfused",
     "attn_unfused_workspace_bytes", "attn_mfma_probe", "attn_strerror",
-    "attn_softmax_derive", "attn_softmax", "attn_gemm_derive", "attn_gemm",
+    "attn_softmax_derive", "attn_softmax", "attn_gemm_derive", "attn_gemm", "attn_fwd_noalloc",
 )
 
 c_int, c_int32, c_int64, c_float, c_double, c_char, c_size_t, c_void_p, c_char_p = (
@@ -130,6 +133,8 @@ def load():
         "attn_fwd_plan": (c_int, [P(HwDesc), c_int, c_int, c_int, c_int, c_int, c_int, P(TileReport)]),
         "attn_fwd": (c_int, [c_void_p, c_void_p, c_void_p, c_void_p, c_int, c_int, c_int, c_int,
                              c_float, c_int, c_int, c_void_p]),
+        "attn_fwd_noalloc": (c_int, [c_void_p, c_void_p, c_void_p, c_void_p, c_int, c_int, c_int, c_int,
+                                     c_float, c_int, c_int, c_void_p]),
         "attn_fwd_workspace_bytes": (c_int, [c_int, c_int, c_int, c_int, c_int, c_int, P(c_size_t)]),
         "attn_fwd_partial": (c_int, [c_void_p, c_void_p, c_void_p, c_void_p, c_int, c_int, c_int, c_int,
                                      c_float, c_int, c_int, c_void_p, c_size_t, c_void_p]),
@@ -250,6 +255,17 @@ def attn_fwd(q, k, v, o, scale: float, causal: bool, stream=None):
             raise AttnError(CODE["ATTN_E_SHAPE"], "q, k, v, o must share shape and dtype")
     _check(load().attn_fwd(_dev_ptr(q), _dev_ptr(k), _dev_ptr(v), _dev_ptr(o), B, H, L, d,
                            float(scale), int(causal), dtype_code(q), _stream_ptr(q, stream)))
+
+
+def attn_fwd_noalloc(q, k, v, o, scale: float, causal: bool, stream=None):
+    """attn_fwd with the split workspace in the library's static per-GPU array
+    (no allocation; calls that overlap on one GPU race on it)."""
+    B, H, L, d = q.shape
+    for t in (k, v, o):
+        if tuple(t.shape) != (B, H, L, d) or t.dtype != q.dtype:
+            raise AttnError(CODE["ATTN_E_SHAPE"], "q, k, v, o must share shape and dtype")
+    _check(load().attn_fwd_noalloc(_dev_ptr(q), _dev_ptr(k), _dev_ptr(v), _dev_ptr(o), B, H, L, d,
+                                   float(scale), int(causal), dtype_code(q), _stream_ptr(q, stream)))
 
 
 def attn_fwd_workspace_bytes(B, H, L, d, causal, dtype) -> int:

@@ -25,6 +25,7 @@ SOURCES = [
     "capi.cpp",
     "tile_derive.cpp",
     "combine.hip",
+    "noalloc.hip",
     "probe.hip",
     "unfused.hip",
     "softmax.hip",

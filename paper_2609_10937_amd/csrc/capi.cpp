@@ -266,6 +266,7 @@ const char* attn_strerror(int status) {
     case ATTN_E_SCALE: return "scale must be finite and >= 0";
     case ATTN_E_ARG: return "invalid argument";
     case ATTN_E_DEVICE: return "current device is not gfx950";
+    case ATTN_E_SCRATCH: return "split workspace larger than the static scratch of attn_fwd_noalloc";
     default: return "unknown status";
   }
 }

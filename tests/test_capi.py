@@ -234,6 +234,19 @@ def test_partial_and_merge_reject_bad_arguments(lib):
     assert lib.attn_fwd_workspace_bytes(1, 1, 16, 64, 0, 0, None) == capi.CODE["ATTN_E_NULLPTR"]
 
 
+def test_noalloc_rejects_bad_arguments(lib):
+    f = lib.attn_fwd_noalloc
+    assert f(None, P, P, P, 1, 1, 16, 64, 0.1, 0, 0, None) == capi.CODE["ATTN_E_NULLPTR"]
+    assert f(P, P + 4, P, P, 1, 1, 16, 64, 0.1, 0, 0, None) == capi.CODE["ATTN_E_ALIGN"]
+    assert f(P, P, P, P, 1, 1, 16, 80, 0.1, 0, 0, None) == capi.CODE["ATTN_E_UNSUPPORTED_D"]
+    assert f(P, P, P, P, 1, 1, 16, 64, -0.1, 0, 0, None) == capi.CODE["ATTN_E_SCALE"]
+    assert f(P, P, P, P, 0, 1, 16, 64, 0.1, 0, 0, None) == capi.CODE["ATTN_E_SHAPE"]
+    with open(os.path.join(ROOT, "include", "attn.h")) as fh:
+        m = re.search(r"#define ATTN_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", fh.read())
+    assert int(m.group(1)) << int(m.group(2)) == capi.NOALLOC_SCRATCH_BYTES
+    assert capi.attn_strerror(capi.CODE["ATTN_E_SCRATCH"]) != "unknown status"
+
+
 def test_probe_rejects_bad_arguments(lib):
     assert lib.attn_mfma_probe(0, None, P, P, None) == capi.CODE["ATTN_E_NULLPTR"]
     assert lib.attn_mfma_probe(5, P, P, P, None) == capi.CODE["ATTN_E_ARG"]
