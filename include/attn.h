@@ -92,9 +92,16 @@ typedef struct {
   int32_t kv_tiles;             /* t_KV x d tiles resident in that share */
   int32_t stage_tiles;          /* t_KV x d tiles staged through registers per step */
   int32_t score_tiles;          /* fp32 t_Q x t_KV score tiles live at once (2 when pipelined) */
+  int32_t p_tiles;              /* t_Q x t_KV tiles of 16-bit weights held in registers for the
+                                   second product (0 when they go through LDS, as in Section 6.1) */
+  int32_t stat_regs;            /* registers per atom-row block of running statistics (the paper's
+                                   (m, delta): 2) */
+  int32_t operand_frags;        /* A-operand fragments of the atom in flight (read ahead of their
+                                   products) */
   int32_t waves_per_wg;
   int32_t waves_per_simd;       /* resident waves per SIMD; divides the register file */
-  int32_t vgpr_fixed;           /* registers per lane outside the counted arrays */
+  int32_t vgpr_fixed;           /* registers per lane outside the counted arrays: lane addresses,
+                                   copy offsets, constants (the paper's instance: 16) */
   int32_t max_split;            /* key-range splits the CU rule may use (1 = none) */
 } attn_op_t;
 

@@ -11,8 +11,10 @@ the paper's CU-centric order (Section 4):
 2. VGPR -> Q tile per wave.  Every array live at the synchronisation point
    between the two GEMMs is counted (Section 6.2, Table 2 caption): the Q
    operand, the fp32 score tile(s), the fp32 output accumulator and the
-   running (m, delta) pair, plus the registers used to stage the next K/V tile
-   and a fixed overhead.  t_Q is the largest multiple of the atom width whose count
+   running (m, delta) pair, plus, for kernel structures that have them, the
+   16-bit weights kept in registers for the second GEMM, more statistics per
+   row block, operand fragments read ahead, the registers used to stage the
+   next K/V tile, and a fixed overhead of addresses and constants.  t_Q is the largest multiple of the atom width whose count
    fits the per-wave budget (Section 4, "VGPR constraint").  The count
    reproduces all four rows of Table 2 with the paper's fp32 instance.
 3. CU count -> grid.  If fewer workgroups than CUs result, the derivation
@@ -68,9 +70,12 @@ class Structure:
     kv_tiles: int = 1        # t_KV x d tiles resident in that share
     stage_tiles: int = 0     # t_KV x d tiles passed through VGPRs per step
     score_tiles: int = 1     # fp32 score tiles live at once (2 when the loop is pipelined)
+    p_tiles: int = 0         # 16-bit weight tiles kept in registers for the second GEMM (0: through LDS)
+    stat_regs: int = 2       # registers of running statistics per atom-row block (m and delta)
+    operand_frags: int = 0   # A-operand fragments of the atom read ahead of their products
     waves_per_wg: int = 1
     waves_per_simd: int = 1  # resident waves per SIMD (divides the register file)
-    vgpr_fixed: int = 16     # addresses, loop state, operand staging
+    vgpr_fixed: int = 16     # addresses, loop state, constants
     max_split: int = 1       # key-range splits allowed by the CU rule
 
 
@@ -84,9 +89,11 @@ def vgpr_count(hw, atom, op, st, t_q, t_kv, n_w):
     q_reg = _cdiv(t_q * op.d * op.elem_bytes, 4 * wf)        # Q operand
     s_reg = st.score_tiles * _cdiv(t_q * t_kv * atom.acc_bytes, 4 * wf)  # score tiles, fp32
     o_reg = _cdiv(t_q * op.d * atom.acc_bytes, 4 * wf)       # output accumulator, fp32
-    stats = 2 * _cdiv(t_q, atom.n)                           # running max and sum
+    p_reg = st.p_tiles * _cdiv(t_q * t_kv * atom.in_bytes, 4 * wf)  # 16-bit weights for the second GEMM
+    stats = st.stat_regs * _cdiv(t_q, atom.n)                # running statistics per row block
+    frags = st.operand_frags * _cdiv(atom.m * atom.k * atom.in_bytes, 4 * wf)  # operands in flight
     stage = _cdiv(st.stage_tiles * t_kv * op.d * op.elem_bytes, 4 * wf * n_w)
-    return q_reg + s_reg + o_reg + stats + stage + st.vgpr_fixed
+    return q_reg + s_reg + o_reg + p_reg + stats + frags + stage + st.vgpr_fixed
 
 
 def derive(hw, atom, op, st):

@@ -38,14 +38,23 @@ namespace {
 
 // Fixed structure of the fused kernel family in fwd_kernel.hpp: all of LDS
 // holds a ring of 5 stages of (K tile, V tile) filled by direct HBM->LDS
-// copies (no registers stage them), one fp32 score tile live at a time, 8
-// waves per workgroup at 2 waves per SIMD.  vgpr_fixed covers what the count
-// does not name (operand fragments in flight, addresses, loop state): the
-// smallest value for which every tile the derivation accepts compiles
-// without spilling (the d=64, 48-rows-per-wave kernel needs more than 256
-// registers, which a fixed term of 83 or more excludes).
+// copies (no registers stage them), 8 waves per workgroup at 2 waves per
+// SIMD.  What a wave holds at the point where the second product of tile
+// j - 1 runs beside the first product of tile j, besides Q, S and O:
+//  - the 16-bit weights of tile j - 1 (kPTiles = 1: P stays in registers);
+//  - per 16-row block, a 4-register row-sum accumulator (the sums come from
+//    a matrix product), the reference point, the check limit and the
+//    pending correction factor (kStatRegs = 7);
+//  - the operand fragment being consumed and the 4 read ahead of it
+//    (kOperandFrags = 5, 4 registers each at the 16x16x32 atom);
+//  - kVgprFixed = 13 counted registers: the lane bases of the K and V
+//    fragment reads (2), the two stage bases of the phase (2), the lane's
+//    chunk offsets of the tile copies (2) and its first copy row (1), the
+//    all-ones A operand of the row-sum product (4), and the lane's query row
+//    and key group for masking (2).
 constexpr int kKvLdsNum = 1, kKvLdsDen = 1, kKvTiles = 10, kStageTiles = 0, kScoreTiles = 1;
-constexpr int kWavesPerWg = 8, kWavesPerSimd = 2, kVgprFixed = 83, kMaxSplit = 16;
+constexpr int kPTiles = 1, kStatRegs = 7, kOperandFrags = 5;
+constexpr int kWavesPerWg = 8, kWavesPerSimd = 2, kVgprFixed = 13, kMaxSplit = 16;
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
@@ -180,6 +189,9 @@ int make_op(int B, int H, int L, int d, int causal, int dtype, attn_op_t* op) {
   op->kv_tiles = kKvTiles;
   op->stage_tiles = kStageTiles;
   op->score_tiles = kScoreTiles;
+  op->p_tiles = kPTiles;
+  op->stat_regs = kStatRegs;
+  op->operand_frags = kOperandFrags;
   op->waves_per_wg = kWavesPerWg;
   op->waves_per_simd = kWavesPerSimd;
   op->vgpr_fixed = kVgprFixed;

@@ -6,9 +6,12 @@
 //      kernel structure gives them (Section 4, LDS constraint).
 //   2. The register budget fixes the query rows per wave, counting every array
 //      live at the synchronisation point between the two products: the Q
-//      operand, the fp32 score tile(s), the fp32 output accumulator and the
-//      running max/sum, plus staging registers and a fixed overhead
-//      (Section 6.2, Table 2 caption; Section 4, VGPR constraint).
+//      operand, the fp32 score tile(s), the fp32 output accumulator, the 16-bit
+//      weights kept for the second product (when they stay in registers), the
+//      running statistics per row block, the operand fragments read ahead of
+//      their products, staging registers, and the kernel family's counted
+//      addresses and constants (Section 6.2, Table 2 caption; Section 4, VGPR
+//      constraint).
 //   3. The CU count bounds the grid from below: split the key range (the
 //      merge of Section 5.3 is associative), then shrink the query tile
 //      (Section 4, occupancy constraint).
@@ -35,9 +38,11 @@ int64_t vgpr_estimate(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, co
   const int64_t q_operand = cdiv(t_q * op->d * op->elem_bytes, lane_words);
   const int64_t scores = op->score_tiles * cdiv(t_q * t_kv * atom->acc_bytes, lane_words);
   const int64_t out_acc = cdiv(t_q * op->d * atom->acc_bytes, lane_words);
-  const int64_t stats = 2 * cdiv(t_q, atom->n);
+  const int64_t weights = op->p_tiles * cdiv(t_q * t_kv * atom->in_bytes, lane_words);
+  const int64_t stats = op->stat_regs * cdiv(t_q, atom->n);
+  const int64_t frags = op->operand_frags * cdiv((int64_t)atom->m * atom->k * atom->in_bytes, lane_words);
   const int64_t staging = cdiv((int64_t)op->stage_tiles * t_kv * op->d * op->elem_bytes, lane_words * n_w);
-  return q_operand + scores + out_acc + stats + staging + op->vgpr_fixed;
+  return q_operand + scores + out_acc + weights + stats + frags + staging + op->vgpr_fixed;
 }
 
 template <typename Report>
@@ -56,7 +61,8 @@ int derive_tiles(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const a
     return ATTN_E_ARG;
   if (op->B <= 0 || op->H <= 0 || op->L <= 0 || op->d <= 0 || op->elem_bytes <= 0) return ATTN_E_ARG;
   if (op->kv_lds_num <= 0 || op->kv_lds_den <= 0 || op->kv_tiles <= 0 || op->stage_tiles < 0 || op->score_tiles < 1 ||
-      op->waves_per_wg <= 0 || op->waves_per_simd <= 0 || op->vgpr_fixed < 0 || op->max_split < 1)
+      op->p_tiles < 0 || op->stat_regs < 0 || op->operand_frags < 0 || op->waves_per_wg <= 0 ||
+      op->waves_per_simd <= 0 || op->vgpr_fixed < 0 || op->max_split < 1)
     return ATTN_E_ARG;
 
   memset(rep, 0, sizeof(*rep));
@@ -93,9 +99,10 @@ int derive_tiles(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const a
   int64_t n_w = op->waves_per_wg;
   const double lw = 4.0 * hw->wavefront_size;
   const double slope = ((double)op->d * op->elem_bytes + (double)op->score_tiles * t_kv * atom->acc_bytes +
-                        (double)op->d * atom->acc_bytes) / lw + 2.0 / atom->n;
+                        (double)op->d * atom->acc_bytes + (double)op->p_tiles * t_kv * atom->in_bytes) / lw +
+                       (double)op->stat_regs / atom->n;
   const double intercept = (double)op->stage_tiles * t_kv * op->d * op->elem_bytes / (lw * n_w) +
-                           op->vgpr_fixed;
+                           (double)op->operand_frags * atom->m * atom->k * atom->in_bytes / lw + op->vgpr_fixed;
   int64_t t_q = 0;
   if (budget > intercept) {
     t_q = (int64_t)((budget - intercept) / slope);

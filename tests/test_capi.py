@@ -54,7 +54,8 @@ def _to_c(hw, atom, op, st):
     a = capi.Atom(m=atom.m, n=atom.n, k=atom.k, in_bytes=atom.in_bytes, acc_bytes=atom.acc_bytes)
     o = capi.Op(B=op.B, H=op.H, L=op.L, d=op.d, elem_bytes=op.elem_bytes, causal=int(op.causal),
                 kv_lds_num=st.kv_lds_num, kv_lds_den=st.kv_lds_den, kv_tiles=st.kv_tiles,
-                stage_tiles=st.stage_tiles, score_tiles=st.score_tiles, waves_per_wg=st.waves_per_wg,
+                stage_tiles=st.stage_tiles, score_tiles=st.score_tiles, p_tiles=st.p_tiles,
+                stat_regs=st.stat_regs, operand_frags=st.operand_frags, waves_per_wg=st.waves_per_wg,
                 waves_per_simd=st.waves_per_simd, vgpr_fixed=st.vgpr_fixed, max_split=st.max_split)
     return h, a, o
 
@@ -80,8 +81,8 @@ def test_table2_through_the_library():
     atom = capi.attn_atom_preset("f32_16x16x4")
     for r in g["table2"]:
         op = capi.Op(B=1, H=1, L=16384, d=r["d"], elem_bytes=4, causal=0, kv_lds_num=1, kv_lds_den=2,
-                     kv_tiles=1, stage_tiles=0, score_tiles=1, waves_per_wg=1, waves_per_simd=1, vgpr_fixed=16,
-                     max_split=1)
+                     kv_tiles=1, stage_tiles=0, score_tiles=1, p_tiles=0, stat_regs=2, operand_frags=0,
+                     waves_per_wg=1, waves_per_simd=1, vgpr_fixed=16, max_split=1)
         rc, rep = capi.attn_tile_derive(hw, atom, op)
         assert rc == 0 and rep.t_kv == r["t_kv"]
         assert capi.attn_vgpr_estimate(hw, atom, op, r["t_q"], r["t_kv"], 1) == r["vgprs"]
@@ -108,7 +109,8 @@ op_s = stg.builds(T.Op, B=stg.integers(1, 8), H=stg.integers(1, 64),
                   elem_bytes=stg.sampled_from([2, 4]), causal=stg.booleans())
 st_s = stg.builds(T.Structure, kv_lds_num=stg.just(1), kv_lds_den=stg.sampled_from([1, 2, 4]),
                   kv_tiles=stg.sampled_from([1, 2, 4, 8]), stage_tiles=stg.sampled_from([0, 1, 2]),
-                  score_tiles=stg.sampled_from([1, 2]),
+                  score_tiles=stg.sampled_from([1, 2]), p_tiles=stg.sampled_from([0, 1, 2]),
+                  stat_regs=stg.integers(0, 8), operand_frags=stg.integers(0, 8),
                   waves_per_wg=stg.sampled_from([1, 2, 4, 8, 16]),
                   waves_per_simd=stg.sampled_from([1, 2, 4]),
                   vgpr_fixed=stg.integers(0, 128), max_split=stg.sampled_from([1, 2, 8, 16]))
@@ -283,14 +285,29 @@ def test_compiled_kernels_fit_without_scratch():
         waves_per_simd = max(1, nw // 4)
         assert r["vgpr"] + r["agpr"] <= 512 // waves_per_simd, name
         assert r["lds"] <= 160 * 1024
-    # the design point the register count's fixed term was calibrated on
+    # The named count of this kernel family: every tile the derivation accepts
+    # at two waves per SIMD is one of the compiled 8-wave instances above (no
+    # scratch, within 256 registers), and one more query block per wave is
+    # refused by counting, at every head dimension.
     hw = capi.attn_hw_desc_preset("gfx950")
-    op = capi.attn_fwd_op(1, 1, 16384, 128, 0, capi.ATTN_BF16)
     atom = capi.attn_atom_preset("bf16_16x16x32")
-    ref = [v for k, v in fwd.items() if "ILi0ELi128ELi64ELi2ELi8ELi5EE" in k][0]
-    assert ref["vgpr"] + ref["agpr"] <= capi.attn_vgpr_estimate(hw, atom, op, 32, 64, 8) <= 256
-    # one more query block per wave is refused by the count (and would spill)
-    assert capi.attn_vgpr_estimate(hw, atom, op, 48, 64, 8) > 256
+    est = {}
+    for d, t_kv, t_q in ((64, 128, 32), (96, 64, 48), (128, 64, 32), (256, 32, 16)):
+        op = capi.attn_fwd_op(1, 1, 16384, d, 0, capi.ATTN_BF16)
+        assert (op.p_tiles, op.stat_regs, op.operand_frags, op.vgpr_fixed) == (1, 7, 5, 13)
+        est[d] = capi.attn_vgpr_estimate(hw, atom, op, t_q, t_kv, 8)
+        assert est[d] <= 256 < capi.attn_vgpr_estimate(hw, atom, op, t_q + 16, t_kv, 8), d
+        r = capi.attn_fwd_plan(1, 1, 16384, d, 0, capi.ATTN_BF16, hw=hw)
+        assert (r.t_kv, r.t_q_wave, r.vgpr_est) == (t_kv, t_q, est[d])
+        tag = f"ILi0ELi{d}ELi{t_kv}ELi{t_q // 16}ELi8ELi5EE"
+        comp = [v for k, v in fwd.items() if tag in k][0]
+        assert comp["scratch"] == 0 and comp["vgpr"] + comp["agpr"] <= 256
+    # d = 128, 32 rows: 32 (Q) + 32 (S) + 64 (O) + 16 (P) + 2 x 7 (statistics)
+    # + 5 x 4 (fragments) + 13 (addresses and constants) = 191
+    assert est[128] == 191
+    # the d = 64, 48-row tile: 24 + 96 + 48 + 48 + 21 + 20 + 13 = 270 > 256
+    op64 = capi.attn_fwd_op(1, 1, 16384, 64, 0, capi.ATTN_BF16)
+    assert capi.attn_vgpr_estimate(hw, atom, op64, 48, 128, 8) == 270
 
 
 def test_one_hip_runtime_after_load():

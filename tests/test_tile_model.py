@@ -111,7 +111,8 @@ op_s = stg.builds(T.Op, B=stg.integers(1, 8), H=stg.integers(1, 64),
                   elem_bytes=stg.sampled_from([2, 4]), causal=stg.booleans())
 st_s = stg.builds(T.Structure, kv_lds_num=stg.just(1), kv_lds_den=stg.sampled_from([1, 2]),
                   kv_tiles=stg.sampled_from([1, 2, 4, 8]), stage_tiles=stg.sampled_from([0, 2]),
-                  score_tiles=stg.sampled_from([1, 2]),
+                  score_tiles=stg.sampled_from([1, 2]), p_tiles=stg.sampled_from([0, 1]),
+                  stat_regs=stg.integers(0, 8), operand_frags=stg.integers(0, 6),
                   waves_per_wg=stg.sampled_from([1, 2, 4, 8]), waves_per_simd=stg.sampled_from([1, 2]),
                   vgpr_fixed=stg.integers(0, 64), max_split=stg.sampled_from([1, 4, 8, 16]))
 
