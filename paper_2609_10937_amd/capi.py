@@ -12,7 +12,8 @@ import ctypes
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libattn.so")
+# ATTN_LIB names another build of this library (the host-sanitizer build of the tests).
+LIB_PATH = os.environ.get("ATTN_LIB") or os.path.join(HERE, "libattn.so")
 
 ATTN_BF16 = 0
 ATTN_F16 = 1
