@@ -80,22 +80,28 @@ def prewarm(fn, min_ms):
 
 def time_steps(fn, steps, warmup, warm_ms=0.0):
     """Warm up (`warmup` calls, then sustained calls until warm_ms of wall time
-    has passed), then time exactly `steps` calls back to back (synchronised
-    before and after, no instrumentation between calls); then the same number
-    of calls again with a HIP event pair around each.  Returns (wall ms per
-    call, event ms per call): the first is the throughput, the second the time
-    each call takes on the stream (events add their own gaps between calls)."""
+    has passed), then time exactly `steps` calls back to back, synchronised
+    before and after, with one HIP event pair on the launch stream around the
+    whole batch and nothing between the calls; then the same number of calls
+    again with an event pair around each (their sorted times go to
+    LAST_EVENT_MS for the median and minimum).  Returns (wall ms per call,
+    batch event ms per call): the first is the throughput, the second the
+    average time a call takes on the stream."""
     import torch
     for _ in range(warmup):
         fn()
     if warm_ms > 0:
         LAST_PREWARM[:] = prewarm(fn, warm_ms)
     torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
+    e0.record()
     for _ in range(steps):
         fn()
+    e1.record()
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) * 1e3 / steps
+    batch = e0.elapsed_time(e1) / steps
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
     for i in range(steps):
@@ -103,9 +109,8 @@ def time_steps(fn, steps, warmup, warm_ms=0.0):
         fn()
         ends[i].record()
     torch.cuda.synchronize()
-    times = sorted(s.elapsed_time(e) for s, e in zip(starts, ends))
-    LAST_EVENT_MS[:] = times
-    return wall, sum(times) / steps
+    LAST_EVENT_MS[:] = sorted(st.elapsed_time(en) for st, en in zip(starts, ends))
+    return wall, batch
 
 
 LAST_EVENT_MS = []  # the per-call event times of the latest time_steps, sorted
@@ -282,6 +287,8 @@ def main():
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the other four workload configurations (tiny f16, 8 heads, batched causal x2)")
     ap.add_argument("--configs", default="1,2,3,5", help="which of the other configurations to run (1-5)")
+    ap.add_argument("--config-steps", type=int, default=0,
+                    help="timed calls per configuration (0: each configuration's own count)")
     ap.add_argument("--no-unfused", action="store_true", help="skip the unfused baseline")
     ap.add_argument("--no-sweep", action="store_true", help="skip the sequence-length sweep (Table 3)")
     ap.add_argument("--no-d256", action="store_true", help="skip the head-dimension-256 workloads")
@@ -327,7 +334,7 @@ def main():
     def kstep():
         capi.attn_fwd_partial(tq, tk, tv, to, w.scale, w.causal, ws)
 
-    _, k_ms = time_steps(kstep, args.steps, args.warmup, 100.0)
+    _, k_ms = time_steps(kstep, args.steps, args.warmup, min(100.0, args.prewarm_ms))
     k_stats = event_stats()
     achieved = fl / (k_ms * 1e-3) / 1e12
     del ws
@@ -359,27 +366,30 @@ def main():
         dt2 = capi.ATTN_BF16 if w2.dtype == "bf16" else capi.ATTN_F16
         t2 = [upload(x, w2.dtype) for x in inputs.workload_inputs(w2)]
         o2 = torch.empty_like(t2[0])
-        _, ev2 = time_steps(lambda: capi.attn_fwd(t2[0], t2[1], t2[2], o2, w2.scale, w2.causal), n_steps, 2, 100.0)
+        warm = min(100.0, args.prewarm_ms)
+        _, ev2 = time_steps(lambda: capi.attn_fwd(t2[0], t2[1], t2[2], o2, w2.scale, w2.causal), n_steps, 2, warm)
         st2 = event_stats()
         nb2 = capi.attn_fwd_workspace_bytes(w2.B, w2.H, w2.L, w2.d, w2.causal, dt2)
         ws2 = torch.empty(max(nb2, 16), dtype=torch.uint8, device="cuda") if nb2 else None
         _, kev2 = time_steps(lambda: capi.attn_fwd_partial(t2[0], t2[1], t2[2], o2, w2.scale, w2.causal, ws2),
-                             n_steps, 2, 50.0)
+                             n_steps, 2, warm / 2)
         kst2 = event_stats()
         p2 = capi.attn_fwd_plan(w2.B, w2.H, w2.L, w2.d, w2.causal, dt2)
         fl2 = flops(w2)
         mc2 = measured_mfma(w2.name)
-        ach = fl2 / (kst2["median_ms"] * 1e-3) / 1e12
+        ach = fl2 / (kev2 * 1e-3) / 1e12
         entry = {"workload": w2.name, "B": w2.B, "H": w2.H, "L": w2.L, "d": w2.d, "dtype": w2.dtype,
                  "causal": w2.causal, "k_scale": w2.k_scale,
-                 "ms": round(st2["median_ms"], 5), "ms_mean": round(ev2, 5), "min_ms": st2["min_ms"],
-                 "tflops": round(fl2 / (st2["median_ms"] * 1e-3) / 1e12, 2),
-                 "pct_peak": round(100 * fl2 / (st2["median_ms"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
+                 "ms": round(ev2, 5), "ms_median_per_call": st2["median_ms"], "min_ms": st2["min_ms"],
+                 "tflops": round(fl2 / (ev2 * 1e-3) / 1e12, 2),
+                 "pct_peak": round(100 * fl2 / (ev2 * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
                  "roofline": {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS,
                               "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 5),
                               "traffic": measured_traffic(w2.name),
-                              "kernel": "fwd_kernel (attn_fwd_partial), HIP events per launch, median",
-                              "kernel_ms": kst2["median_ms"], "kernel_ms_min": kst2["min_ms"],
+                              "kernel": "fwd_kernel (attn_fwd_partial): one HIP event pair around the "
+                                        "back-to-back timed launches, per launch",
+                              "kernel_ms": round(kev2, 5), "kernel_ms_median_per_call": kst2["median_ms"],
+                              "kernel_ms_min": kst2["min_ms"],
                               "frac_at_counter_clock": at_clock(ach, mc2), "mfma_counters": mc2},
                  "algorithmic_flops": fl2, "algorithmic_bytes": fused_bytes(w2),
                  "tiles": {"t_kv": p2.t_kv, "t_q_wave": p2.t_q_wave, "n_waves": p2.n_waves,
@@ -390,11 +400,10 @@ def main():
                               device="cuda")
             ou = torch.empty_like(o2)
             _, uev = time_steps(lambda: capi.attn_fwd_unfused(t2[0], t2[1], t2[2], ou, w2.scale, w2.causal, wsu),
-                                n_steps, 2, 50.0)
-            ust = event_stats()
-            entry["unfused"] = {"ms": round(ust["median_ms"], 5),
-                                "tflops": round(fl2 / (ust["median_ms"] * 1e-3) / 1e12, 2),
-                                "speedup_fused_over_unfused": round(ust["median_ms"] / st2["median_ms"], 3),
+                                n_steps, 2, warm / 2)
+            entry["unfused"] = {"ms": round(uev, 5),
+                                "tflops": round(fl2 / (uev * 1e-3) / 1e12, 2),
+                                "speedup_fused_over_unfused": round(uev / ev2, 3),
                                 "algorithmic_bytes": unfused_bytes(w2),
                                 "bytes_ratio": round(unfused_bytes(w2) / fused_bytes(w2), 3),
                                 "measured_bytes": measured_unfused_bytes(w2.name)}
@@ -416,7 +425,7 @@ def main():
                 configs.append({"config": i, "workload": name, "headline": True})
                 continue
             print(f"bench: config {i} {name}", file=sys.stderr, flush=True)
-            configs.append({"config": i, **config_leg(inputs.WORKLOADS[name], n_steps,
+            configs.append({"config": i, **config_leg(inputs.WORKLOADS[name], args.config_steps or n_steps,
                                                       with_unfused=name == "h8_l1024_d128")})
 
     sweep = None
@@ -429,7 +438,8 @@ def main():
             print(f"bench: sweep L={ws_w.L}", file=sys.stderr, flush=True)
             ts = [upload(x, ws_w.dtype) for x in inputs.workload_inputs(ws_w)]
             tos = torch.empty_like(ts[0])
-            _, f_ms = time_steps(lambda: capi.attn_fwd(ts[0], ts[1], ts[2], tos, ws_w.scale, ws_w.causal), 20, 20)
+            _, f_ms = time_steps(lambda: capi.attn_fwd(ts[0], ts[1], ts[2], tos, ws_w.scale, ws_w.causal), 20, 20,
+                                 min(50.0, args.prewarm_ms))
             wsu = torch.empty(capi.attn_unfused_workspace_bytes(1, 1, ws_w.L, capi.ATTN_BF16), dtype=torch.uint8,
                               device="cuda")
             _, u_ms = time_steps(lambda: capi.attn_fwd_unfused(ts[0], ts[1], ts[2], tos, ws_w.scale, ws_w.causal,
@@ -450,7 +460,8 @@ def main():
             t3 = [upload(x, w3.dtype) for x in inputs.workload_inputs(w3)]
             o3 = torch.empty_like(t3[0])
             n3 = 20 if w3.B * w3.H == 1 else 5
-            _, ev3 = time_steps(lambda: capi.attn_fwd(t3[0], t3[1], t3[2], o3, w3.scale, w3.causal), n3, n3)
+            _, ev3 = time_steps(lambda: capi.attn_fwd(t3[0], t3[1], t3[2], o3, w3.scale, w3.causal), n3, n3,
+                                min(50.0, args.prewarm_ms))
             p3 = capi.attn_fwd_plan(w3.B, w3.H, w3.L, w3.d, w3.causal, capi.ATTN_BF16)
             out.append({"workload": w3.name, "ms": round(ev3, 4),
                         "tflops": round(flops(w3) / (ev3 * 1e-3) / 1e12, 1),
@@ -566,7 +577,8 @@ def main():
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 5),
                      "traffic": measured_traffic(w.name),
-                     "kernel": "fwd_kernel (attn_fwd_partial), HIP events per launch",
+                     "kernel": "fwd_kernel (attn_fwd_partial): one HIP event pair around the back-to-back timed "
+                               "launches on their stream, per launch",
                      "kernel_ms": round(k_ms, 5), "kernel_ms_median": k_stats["median_ms"],
                      "kernel_ms_min": k_stats["min_ms"], "step_event_ms": round(ev_ms, 5),
                      "frac_at_counter_clock": at_clock(achieved, measured_mfma(w.name)),
