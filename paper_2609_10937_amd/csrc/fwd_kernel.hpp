@@ -68,6 +68,7 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef short i16x8_t __attribute__((ext_vector_type(8)));
+typedef int32_t i32x4_t __attribute__((ext_vector_type(4)));
 
 #define ATTN_LDS __attribute__((address_space(3)))
 #define ATTN_GLOBAL __attribute__((address_space(1)))
@@ -141,6 +142,27 @@ __device__ __forceinline__ uint64_t uniform_ptr(const void* p) {
 }
 __device__ __forceinline__ void copy_to_lds(const void* base, uint32_t off, uint32_t lds_dst) {
   asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(uniform_ptr(base)),
+               "s"(__builtin_amdgcn_readfirstlane(lds_dst))
+               : "memory", "m0");
+}
+// Buffer resource (a gfx9 V#) over `bytes` bytes from `base`: raw (stride 0,
+// no swizzle), so a lane whose offset is at or past `bytes` reads zeros and
+// touches no memory.  Built from wave-uniform values; the fields pass
+// through readfirstlane so that the descriptor lives in scalar registers.
+__device__ __forceinline__ i32x4_t buffer_rsrc(uint64_t base, uint32_t bytes) {
+  i32x4_t r;
+  r[0] = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)base);
+  r[1] = __builtin_amdgcn_readfirstlane((int32_t)((uint32_t)(base >> 32) & 0xffffu));
+  r[2] = __builtin_amdgcn_readfirstlane((int32_t)bytes);
+  r[3] = 0x00020000;  // 32-bit data format, no swizzle, no index stride
+  return r;
+}
+// One 16-byte-per-lane copy from a buffer straight into LDS
+// (buffer_load_dwordx4 ... lds): lane l's 16 bytes at byte offset `off` of
+// the buffer land at LDS byte address lds_dst + 16 l, zeros for a lane past
+// the buffer's end.  Inline assembly for the same reason as copy_to_lds.
+__device__ __forceinline__ void copy_to_lds_buf(i32x4_t rsrc, uint32_t off, uint32_t lds_dst) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds" ::"v"(off), "s"(rsrc),
                "s"(__builtin_amdgcn_readfirstlane(lds_dst))
                : "memory", "m0");
 }
@@ -395,47 +417,62 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   // row P/KCH, logical chunk (P%KCH) ^ swizzle(row).  Block b of a tile image
   // (1 KB) holds rows b*RPB .. b*RPB + RPB - 1; copying wave cw takes blocks
   // cw, cw + NCW, cw + 2 NCW, ..., so block i of a lane sits at row
-  // r0 + i NCW RPB.  Each copy is the head's base address (wave-uniform) plus
-  // a lane offset: source row min(kv0 + row, L - 1) -- rows past the end of
-  // the sequence repeat row L-1 (finite data that the mask removes), so every
-  // tile, and every tile index, takes the same branch-free path -- and the
-  // byte offset of the lane's chunk within the row.  When NCW * RPB is a
-  // multiple of 16 rows (the period of both swizzles) the chunk offsets of
-  // all of a lane's blocks coincide.
+  // r0 + i NCW RPB.  Each copy reads through a buffer descriptor whose base is
+  // the tile's first row and whose size covers the rows of this workgroup's
+  // key range that the tile holds (none for tiles past the range), so a
+  // lane's byte offset within the tile is the same for every tile and rows
+  // past the range or the sequence arrive as zeros (finite; the mask removes
+  // their keys) without touching memory.  When NCW * RPB is a multiple of
+  // 16 rows (the period of both swizzles) the chunk offsets of all of a
+  // lane's blocks coincide.
   constexpr int RPB = 1024 / ROWB;
   constexpr bool SHIFT = (NCW * RPB) % 16 == 0;
-  constexpr int NCB = SHIFT ? 1 : LPW;
   const int cw = w;  // index among the copying waves
   const uint32_t r0 = (uint32_t)((cw * 64 + lane) / KCH);
-  uint32_t kcb[NCB], vcb[NCB];
-#pragma unroll
-  for (int i = 0; i < NCB; ++i) {
+  // A lane's byte offset within a tile for its block i of K (V = false) or
+  // V: loop-invariant registers when the blocks share their chunk offsets
+  // (the 4- and 8-wave kernels), else formed at each copy.
+  auto block_off = [&](int i, bool is_v) ATTN_INLINE -> uint32_t {
     const int r = (int)r0 + i * NCW * RPB, pc = lane % KCH;
-    if constexpr (D == DL) {
-      kcb[i] = (uint32_t)((pc ^ k_swz<KCH>(r)) * 16);
-      vcb[i] = (uint32_t)((pc ^ v_swz<KCH>(r)) * 16);
-    } else {
-      kcb[i] = (uint32_t)(min(pc ^ k_swz<KCH>(r), D / 8 - 1) * 16);
-      vcb[i] = (uint32_t)(min(pc ^ v_swz<KCH>(r), D / 8 - 1) * 16);
-    }
+    int ch = pc ^ (is_v ? v_swz<KCH>(r) : k_swz<KCH>(r));
+    if constexpr (D != DL) ch = min(ch, D / 8 - 1);
+    return (uint32_t)(r * GROWB + ch * 16);
+  };
+  constexpr int NOFF = SHIFT ? LPW : 1;
+  uint32_t koff[NOFF], voff[NOFF];
+#pragma unroll
+  for (int i = 0; i < NOFF; ++i) {
+    koff[i] = block_off(i, false);
+    voff[i] = block_off(i, true);
   }
+  const uint64_t kh_base = uniform_ptr(Kh), vh_base = uniform_ptr(Vh);
+  // Key rows this workgroup reads: its split's range, clipped to the sequence.
+  const int kv_end = __builtin_amdgcn_readfirstlane(min(L, (t_begin + max(n, 0)) * TKV));
   // This wave's part of tile j: its LPW blocks of the K image and of the V
   // image, as copies 0 .. NC-1 (copy 2i is block i of K, 2i+1 block i of V);
   // issue(j, lo, hi) makes copies lo .. hi-1.
   constexpr int NC = 2 * LPW;
-  // 32-bit lane offsets reach every row: the host admits L * d * 2 <= 2^32.
-  auto issue = [&](int j, int lo, int hi) ATTN_INLINE {
-    const uint32_t kv0 = (uint32_t)((t_begin + j) * TKV);
+  // The K and V buffer descriptors of tile j.
+  struct TileRsrc {
+    i32x4_t k, v;
+  };
+  auto tile_rsrc = [&](int j) ATTN_INLINE -> TileRsrc {
+    const int kv0 = (t_begin + j) * TKV;
+    const uint32_t bytes = (uint32_t)max(0, min(kv_end - kv0, TKV)) * GROWB;
+    return TileRsrc{buffer_rsrc(kh_base + (uint64_t)kv0 * GROWB, bytes),
+                    buffer_rsrc(vh_base + (uint64_t)kv0 * GROWB, bytes)};
+  };
+  auto issue_r = [&](const TileRsrc& rs, int j, int lo, int hi) ATTN_INLINE {
+    const i32x4_t kr = rs.k, vr = rs.v;
     const uint32_t kdst = (uint32_t)__builtin_amdgcn_readfirstlane(lds0 + (j % ST) * STAGEB) + cw * 1024;
-    const uint32_t t = kv0 + r0;
 #pragma unroll
     for (int ci = lo; ci < hi; ++ci) {
       const int i = ci >> 1;
-      const uint32_t row = min(t + (uint32_t)(i * NCW * RPB), (uint32_t)(L - 1));
-      if (ci & 1) copy_to_lds(Vh, row * GROWB + vcb[SHIFT ? 0 : i], kdst + TILEB + i * NCW * 1024);
-      else copy_to_lds(Kh, row * GROWB + kcb[SHIFT ? 0 : i], kdst + i * NCW * 1024);
+      if (ci & 1) copy_to_lds_buf(vr, SHIFT ? voff[i % NOFF] : block_off(i, true), kdst + TILEB + i * NCW * 1024);
+      else copy_to_lds_buf(kr, SHIFT ? koff[i % NOFF] : block_off(i, false), kdst + i * NCW * 1024);
     }
   };
+  auto issue = [&](int j, int lo, int hi) ATTN_INLINE { issue_r(tile_rsrc(j), j, lo, hi); };
   // This wave's copies of tile j are complete once no more than the copies
   // of the tiles requested after it are outstanding (vector-memory
   // operations retire in issue order).
@@ -539,6 +576,8 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
     constexpr int F = (G2 ? NVF : 0) + (G1 ? NKF : 0);
     const uint32_t Vs = vbase + (uint32_t)__builtin_amdgcn_readfirstlane(lds0 + ((j + ST - 1) % ST) * STAGEB + TILEB);
     const uint32_t Ks = kbase + (uint32_t)__builtin_amdgcn_readfirstlane(lds0 + (j % ST) * STAGEB);
+    TileRsrc crs{};
+    if constexpr (G1) crs = tile_rsrc(jc);
     auto load = [&](int f) ATTN_INLINE -> V8 {
       if (G2 && f < NVF) return load_v(Vs, f / NDB, f % NDB);
       const int fk = f - (G2 ? NVF : 0);
@@ -583,7 +622,7 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
       if constexpr (G1) {
 #pragma unroll
         for (int ci = 0; ci < NC; ++ci)
-          if (f == (2 * ci + 1) * F / (2 * NC)) issue(jc, ci, ci + 1);
+          if (f == (2 * ci + 1) * F / (2 * NC)) issue_r(crs, jc, ci, ci + 1);
       }
     }
     // Keep that order through instruction scheduling: the first PF
