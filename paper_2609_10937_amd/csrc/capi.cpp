@@ -47,14 +47,15 @@ namespace {
 //    pending correction factor (kStatRegs = 7);
 //  - the operand fragment being consumed and the 4 read ahead of it
 //    (kOperandFrags = 5, 4 registers each at the 16x16x32 atom);
-//  - kVgprFixed = 13 counted registers: the lane bases of the K and V
+//  - kVgprFixed = 14 counted registers: the lane bases of the K and V
 //    fragment reads (2), the two stage bases of the phase (2), the lane's
-//    chunk offsets of the tile copies (2) and its first copy row (1), the
-//    all-ones A operand of the row-sum product (4), and the lane's query row
-//    and key group for masking (2).
+//    byte offsets within a tile for its two K and two V copies (4; the
+//    copies read through per-tile buffer descriptors, so the offsets do not
+//    change from tile to tile), the all-ones A operand of the row-sum
+//    product (4), and the lane's query row and key group for masking (2).
 constexpr int kKvLdsNum = 1, kKvLdsDen = 1, kKvTiles = 10, kStageTiles = 0, kScoreTiles = 1;
 constexpr int kPTiles = 1, kStatRegs = 7, kOperandFrags = 5;
-constexpr int kWavesPerWg = 8, kWavesPerSimd = 2, kVgprFixed = 13, kMaxSplit = 16;
+constexpr int kWavesPerWg = 8, kWavesPerSimd = 2, kVgprFixed = 14, kMaxSplit = 16;
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
