@@ -510,6 +510,12 @@ def main():
         gc = torch.empty((M, N), dtype=torch.float32, device="cuda")
         _, g_ms = time_steps(lambda: capi.attn_gemm(ga, gb, gc), 50, 50)
         _, t_ms = time_steps(lambda: torch.mm(ga, gb), 50, 50)
+        # The same product with fp32 output (this operator's output type), where
+        # the installed torch offers it.
+        try:
+            _, t32_ms = time_steps(lambda: torch.mm(ga, gb, out_dtype=torch.float32), 50, 50)
+        except (RuntimeError, TypeError, NotImplementedError):
+            t32_ms = None
         gfl = 2.0 * M * N * K
         gc_ = measured_gemm_counters()
         gemm = {"M": M, "N": N, "K": K, "dtype": "bf16", "out": "f32", "us": round(1e3 * g_ms, 2),
@@ -524,6 +530,8 @@ def main():
                              "clock_ghz": None if gc_ is None else gc_["clock_ghz"]},
                 "torch_mm_bf16_us": round(1e3 * t_ms, 2),
                 "torch_mm_tflops": round(gfl / (t_ms * 1e-3) / 1e12, 1),
+                "torch_mm_f32_out_us": None if t32_ms is None else round(1e3 * t32_ms, 2),
+                "torch_mm_f32_out_tflops": None if t32_ms is None else round(gfl / (t32_ms * 1e-3) / 1e12, 1),
                 "tiles": {"t_m": rep.t_m, "t_n": rep.t_n, "t_k": rep.t_k, "warp_m": rep.warp_m,
                           "warp_n": rep.warp_n, "grid": rep.grid, "vgpr_est": rep.vgpr_est,
                           "binding": rep.binding.decode()}}
