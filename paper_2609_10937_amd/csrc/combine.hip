@@ -17,11 +17,12 @@ __device__ __forceinline__ float widen(uint16_t h) {
   else return (float)__builtin_bit_cast(_Float16, h);
 }
 
-// NS is a compile-time bound on the split count (2, 4, 8 or 16), so each
-// thread's loads (NS reference/sum pairs and NS 16-byte partials) issue
-// together.  Slots past the actual count n re-read split n - 1 (cache hits)
-// and take weight 0, which leaves the maximum, the sum and the accumulator
-// unchanged.
+// NS is a compile-time bound on the split count (2, 4, 8 or 16).  Every
+// thread first issues all of its loads (NS reference/sum pairs as one 8-byte
+// load each and NS 16-byte partials) and only then does arithmetic, so the
+// loads overlap instead of waiting for each other one split at a time.  Slots
+// past the actual count n re-read split n - 1 (cache hits) and take weight 0,
+// which leaves the maximum, the sum and the accumulator unchanged.
 template <int DT, int D, int NS>
 __global__ void __launch_bounds__(256) combine_kernel(const FwdParams p) {
   using S = typename Mfma<DT>::S;
@@ -33,24 +34,33 @@ __global__ void __launch_bounds__(256) combine_kernel(const FwdParams p) {
   const int64_t row = idx / OCTS;
   const int d8 = (int)(idx - row * OCTS);
   const int64_t stride = rows;  // rows per split
+  const float2* __restrict__ ml = reinterpret_cast<const float2*>(p.part_ml);
+  const uint16_t* __restrict__ part = static_cast<const uint16_t*>(p.part_o);
+
+  float2 st[NS];
+  u32x4_t po[NS];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    const int64_t sr = min(s, n_split - 1) * stride + row;
+    st[s] = ml[sr];
+    po[s] = *reinterpret_cast<const u32x4_t*>(part + sr * D + 8 * d8);
+  }
+  // Keep the scheduler from sinking loads below this point.
+  __builtin_amdgcn_sched_barrier(0);
 
   float m = -INFINITY;
 #pragma unroll
-  for (int s = 0; s < NS; ++s) m = fmaxf(m, p.part_ml[(min(s, n_split - 1) * stride + row) * 2]);
+  for (int s = 0; s < NS; ++s) m = fmaxf(m, st[s].x);
   float lt = 0.f;
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
-    const int64_t sr = min(s, n_split - 1) * stride + row;
-    const float ms = p.part_ml[sr * 2];
-    const float ls = p.part_ml[sr * 2 + 1];
-    const float wgt = (s >= n_split || ms == -INFINITY) ? 0.f : ls * exp2_hw(ms - m);
+    const float wgt = (s >= n_split || st[s].x == -INFINITY) ? 0.f : st[s].y * exp2_hw(st[s].x - m);
     lt += wgt;
-    const u32x4_t po = *reinterpret_cast<const u32x4_t*>(static_cast<const uint16_t*>(p.part_o) + sr * D + 8 * d8);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      acc[2 * e] += wgt * widen<DT>((uint16_t)(po[e] & 0xffffu));
-      acc[2 * e + 1] += wgt * widen<DT>((uint16_t)(po[e] >> 16));
+      acc[2 * e] += wgt * widen<DT>((uint16_t)(po[s][e] & 0xffffu));
+      acc[2 * e + 1] += wgt * widen<DT>((uint16_t)(po[s][e] >> 16));
     }
   }
   const float inv = lt > 0.f ? 1.f / lt : 0.f;
