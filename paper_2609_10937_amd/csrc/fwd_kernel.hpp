@@ -365,9 +365,13 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   // and runs them xg at a time, ranks outermost within such a group: the
   // workgroups an XCD runs together then stream the same K/V tiles through
   // its L2.  A group holds at least 64 query tiles (two per CU of an XCD) so
-  // that heavy and light causal tiles still balance.  Causal launches heavy
-  // tiles (high ranks of the query order) first.  Otherwise the plain order:
-  // units fastest within a rank.
+  // that heavy and light causal tiles still balance.  Otherwise, with a split
+  // key range, all splits of a query tile go to one XCD (tile t, counted
+  // head-major, on XCD t % 8), so its L2 fetches the tile's Q rows once
+  // instead of once per split: every workgroup loads Q at the start, where
+  // its key tiles follow over the whole loop.  Causal launches heavy tiles
+  // (high ranks of the query order) first.  Otherwise the plain order: units
+  // fastest within a rank.
   const int units = p.BH * p.n_split;
   int xg = 1;
   while (xg * p.n_qt < 64) xg *= 2;
@@ -378,6 +382,13 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
     const int gi = i / per_group, r = i - gi * per_group;
     rank = r / xg;
     unit = x + 8 * (gi * xg + (r - rank * xg));
+  } else if (p.n_split > 1 && (p.BH * p.n_qt) % 8 == 0) {
+    const int x = blockIdx.x % 8, i = blockIdx.x / 8;
+    const int sp = i % p.n_split;
+    const int t = (i / p.n_split) * 8 + x;
+    const int hd = t / p.n_qt;
+    rank = t - hd * p.n_qt;
+    unit = hd * p.n_split + sp;
   } else {
     rank = blockIdx.x / units;
     unit = blockIdx.x - rank * units;
