@@ -249,6 +249,7 @@ int prepare(const void* Q, const void* K, const void* V, void* O, int B, int H, 
   p.tiles_per_split = (n_kv + out->rep.n_split - 1) / out->rep.n_split;
   p.causal = causal != 0;
   p.c = scale * 1.4426950408889634f;
+  p.tile_q = out->rep.tile_q;
   const size_t rows = (size_t)p.n_split * p.BH * L;
   out->ws_bytes = p.n_split > 1 ? rows * (size_t)d * 2 + rows * 8 : 0;
   return ATTN_OK;

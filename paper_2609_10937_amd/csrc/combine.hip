@@ -17,22 +17,41 @@ __device__ __forceinline__ float widen(uint16_t h) {
   else return (float)__builtin_bit_cast(_Float16, h);
 }
 
+// When the fused kernel ran every split of query tile t on XCD t % 8
+// (kOrderTiles), BY_TILE orders the merge's workgroups the same way: the
+// chunks of 256 (row, octet) items of tile t run on XCD t % 8, whose L2 still
+// holds the partials that XCD wrote.  Otherwise one flat order.
+//
 // NS is a compile-time bound on the split count (2, 4, 8 or 16).  Every
 // thread first issues all of its loads (NS reference/sum pairs as one 8-byte
 // load each and NS 16-byte partials) and only then does arithmetic, so the
 // loads overlap instead of waiting for each other one split at a time.  Slots
 // past the actual count n re-read split n - 1 (cache hits) and take weight 0,
 // which leaves the maximum, the sum and the accumulator unchanged.
-template <int DT, int D, int NS>
+template <int DT, int D, int NS, bool BY_TILE>
 __global__ void __launch_bounds__(256) combine_kernel(const FwdParams p) {
   using S = typename Mfma<DT>::S;
   constexpr int OCTS = D / 8;
   const int n_split = p.n_split;
   const int64_t rows = (int64_t)p.BH * p.L;
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= rows * OCTS) return;
-  const int64_t row = idx / OCTS;
-  const int d8 = (int)(idx - row * OCTS);
+  int64_t row;
+  int d8;
+  if constexpr (BY_TILE) {
+    const int wpt = p.tile_q * OCTS / 256;  // workgroups per query tile
+    const int x = blockIdx.x % 8, i = blockIdx.x / 8;
+    const int t = (i / wpt) * 8 + x;
+    const int hd = t / p.n_qt, rank = t - hd * p.n_qt;
+    const int item = (i - (i / wpt) * wpt) * 256 + threadIdx.x;
+    const int q = rank * p.tile_q + item / OCTS;
+    if (q >= p.L) return;
+    row = (int64_t)hd * p.L + q;
+    d8 = item % OCTS;
+  } else {
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= rows * OCTS) return;
+    row = idx / OCTS;
+    d8 = (int)(idx - row * OCTS);
+  }
   const int64_t stride = rows;  // rows per split
   const float2* __restrict__ ml = reinterpret_cast<const float2*>(p.part_ml);
   const uint16_t* __restrict__ part = static_cast<const uint16_t*>(p.part_o);
@@ -73,29 +92,40 @@ __global__ void __launch_bounds__(256) combine_kernel(const FwdParams p) {
   *reinterpret_cast<u32x4_t*>(static_cast<uint16_t*>(p.o) + row * D + 8 * d8) = (u32x4_t){out[0], out[1], out[2], out[3]};
 }
 
+template <int DT, int D, bool BY_TILE>
+static void launch_combine_o(const FwdParams& p, unsigned grid, hipStream_t s) {
+  if (p.n_split <= 2) hipLaunchKernelGGL((combine_kernel<DT, D, 2, BY_TILE>), dim3(grid), dim3(256), 0, s, p);
+  else if (p.n_split <= 4) hipLaunchKernelGGL((combine_kernel<DT, D, 4, BY_TILE>), dim3(grid), dim3(256), 0, s, p);
+  else if (p.n_split <= 8) hipLaunchKernelGGL((combine_kernel<DT, D, 8, BY_TILE>), dim3(grid), dim3(256), 0, s, p);
+  else hipLaunchKernelGGL((combine_kernel<DT, D, 16, BY_TILE>), dim3(grid), dim3(256), 0, s, p);
+}
+
 template <int DT, int D>
-static void launch_combine_d(const FwdParams& p, unsigned grid, hipStream_t s) {
-  if (p.n_split <= 2) hipLaunchKernelGGL((combine_kernel<DT, D, 2>), dim3(grid), dim3(256), 0, s, p);
-  else if (p.n_split <= 4) hipLaunchKernelGGL((combine_kernel<DT, D, 4>), dim3(grid), dim3(256), 0, s, p);
-  else if (p.n_split <= 8) hipLaunchKernelGGL((combine_kernel<DT, D, 8>), dim3(grid), dim3(256), 0, s, p);
-  else hipLaunchKernelGGL((combine_kernel<DT, D, 16>), dim3(grid), dim3(256), 0, s, p);
+static void launch_combine_d(const FwdParams& p, bool by_tile, unsigned grid, hipStream_t s) {
+  if (by_tile) launch_combine_o<DT, D, true>(p, grid, s);
+  else launch_combine_o<DT, D, false>(p, grid, s);
 }
 
 template <int DT>
-static void launch_combine_t(const FwdParams& p, int d, unsigned grid, hipStream_t s) {
-  if (d == 256) launch_combine_d<DT, 256>(p, grid, s);
-  else if (d == 128) launch_combine_d<DT, 128>(p, grid, s);
-  else if (d == 96) launch_combine_d<DT, 96>(p, grid, s);
-  else launch_combine_d<DT, 64>(p, grid, s);
+static void launch_combine_t(const FwdParams& p, int d, bool by_tile, unsigned grid, hipStream_t s) {
+  if (d == 256) launch_combine_d<DT, 256>(p, by_tile, grid, s);
+  else if (d == 128) launch_combine_d<DT, 128>(p, by_tile, grid, s);
+  else if (d == 96) launch_combine_d<DT, 96>(p, by_tile, grid, s);
+  else launch_combine_d<DT, 64>(p, by_tile, grid, s);
 }
 
 hipError_t launch_combine(const FwdParams& p, int d, int dtype, hipStream_t s) {
   if (p.n_split < 1 || p.n_split > 16) return hipErrorInvalidValue;  // the largest compiled bound
-  const int64_t threads = (int64_t)p.BH * p.L * (d / 8);
-  const int64_t grid = (threads + 255) / 256;
+  int xg;
+  // Tile order needs whole 256-item chunks per query tile and tiles that
+  // cover the sequence.
+  const bool by_tile = fwd_order(p.BH, p.n_qt, p.n_split, &xg) == kOrderTiles && p.tile_q > 0 &&
+                       (p.tile_q * (d / 8)) % 256 == 0 && (int64_t)p.n_qt * p.tile_q >= p.L;
+  const int64_t grid = by_tile ? (int64_t)p.BH * p.n_qt * (p.tile_q * (d / 8) / 256)
+                               : ((int64_t)p.BH * p.L * (d / 8) + 255) / 256;
   if (grid > 0x7fffffffLL) return hipErrorInvalidValue;
-  if (dtype == ATTN_BF16) launch_combine_t<ATTN_BF16>(p, d, (unsigned)grid, s);
-  else launch_combine_t<ATTN_F16>(p, d, (unsigned)grid, s);
+  if (dtype == ATTN_BF16) launch_combine_t<ATTN_BF16>(p, d, by_tile, (unsigned)grid, s);
+  else launch_combine_t<ATTN_F16>(p, d, by_tile, (unsigned)grid, s);
   return hipGetLastError();
 }
 

@@ -373,16 +373,16 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   // (high ranks of the query order) first.  Otherwise the plain order: units
   // fastest within a rank.
   const int units = p.BH * p.n_split;
-  int xg = 1;
-  while (xg * p.n_qt < 64) xg *= 2;
+  int xg;
+  const FwdOrder order = fwd_order(p.BH, p.n_qt, p.n_split, &xg);
   int unit, rank;
-  if (units % (8 * xg) == 0) {
+  if (order == kOrderUnits) {
     const int x = blockIdx.x % 8, i = blockIdx.x / 8;
     const int per_group = xg * p.n_qt;
     const int gi = i / per_group, r = i - gi * per_group;
     rank = r / xg;
     unit = x + 8 * (gi * xg + (r - rank * xg));
-  } else if (p.n_split > 1 && (p.BH * p.n_qt) % 8 == 0) {
+  } else if (order == kOrderTiles) {
     const int x = blockIdx.x % 8, i = blockIdx.x / 8;
     const int sp = i % p.n_split;
     const int t = (i / p.n_split) * 8 + x;

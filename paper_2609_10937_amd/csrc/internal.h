@@ -23,7 +23,25 @@ struct FwdParams {
   int tiles_per_split;  // key tiles per split
   int causal;
   float c;              // scale * log2(e): exp(scale*(x - m)) = exp2(c*(x - m))
+  int tile_q;           // query rows per workgroup of the fused kernel
 };
+
+// The fused kernel's workgroup order (the XCD a workgroup runs on is its
+// index mod 8), decided alike on the host and the device:
+//   kOrderUnits   units (head, split) spread over the XCDs, xg at a time;
+//   kOrderTiles   with a split key range, all splits of query tile t
+//                 (counted head-major) on XCD t % 8;
+//   kOrderPlain   units fastest within a query rank.
+// xg is the smallest power of two with xg * n_qt >= 64.
+enum FwdOrder { kOrderUnits, kOrderTiles, kOrderPlain };
+__host__ __device__ inline FwdOrder fwd_order(int BH, int n_qt, int n_split, int* xg_out) {
+  int xg = 1;
+  while (xg * n_qt < 64) xg *= 2;
+  *xg_out = xg;
+  if ((BH * n_split) % (8 * xg) == 0) return kOrderUnits;
+  if (n_split > 1 && (BH * n_qt) % 8 == 0) return kOrderTiles;
+  return kOrderPlain;
+}
 
 using FwdLaunch = hipError_t (*)(const FwdParams&, unsigned grid, hipStream_t);
 
