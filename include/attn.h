@@ -112,7 +112,10 @@ typedef struct {
   int32_t t_q_wave;             /* query rows per wave (fixed by registers) */
   int32_t n_waves;              /* waves per workgroup */
   int32_t tile_q;               /* query rows per workgroup = n_waves * t_q_wave */
-  int32_t n_split;              /* key-range splits (1 = none) */
+  int32_t n_split;              /* key-range splits (1 = none); causal: the most pieces of one
+                                   query tile's key range */
+  int32_t tiles_per_split;      /* key tiles per split (causal: per piece of a query tile's own
+                                   key range, the last piece of a tile holding the rest) */
   int64_t grid;                 /* workgroups launched by the fused kernel */
   int32_t vgpr_est, vgpr_budget;/* registers per lane at the GEMM1/GEMM2 sync point */
   int64_t lds_used, lds_budget;

@@ -99,7 +99,7 @@ def vgpr_count(hw, atom, op, st, t_q, t_kv, n_w):
 def derive(hw, atom, op, st):
     """Return a dict with the tiles, the grid and the feasibility report."""
     rep = dict(feasible=False, binding="", t_kv=0, t_q_wave=0, n_waves=0, tile_q=0,
-               n_split=1, grid=0, vgpr_est=0, vgpr_budget=0, lds_used=0, lds_budget=0,
+               n_split=1, tiles_per_split=0, grid=0, vgpr_est=0, vgpr_budget=0, lds_used=0, lds_budget=0,
                wg_per_cu=0.0, low_occupancy=True, lds_bw_ok=True)
     align_kv = math.lcm(atom.n, atom.k)
     align_q = atom.n
@@ -173,9 +173,37 @@ def derive(hw, atom, op, st):
         n_qt = _cdiv(op.L, n_w * t_q)
         binding = "CU"
 
+    tile_q = n_w * t_q
+    per = _cdiv(n_kv, n_split)
     grid = heads * n_qt * n_split
-    rep.update(feasible=True, binding=binding, t_q_wave=t_q, n_waves=n_w, tile_q=n_w * t_q,
-               n_split=n_split, grid=grid,
+    if op.causal and n_split > 1 and tile_q % t_kv == 0:
+        # Causal (our addition): query tile qt sees only its first
+        # min(n_kv, ceil(min(L, (qt+1) tile_q) / t_kv)) key tiles, so fixed
+        # key ranges leave the early tiles' later splits empty and give the
+        # last tiles all the work.  Instead each query tile's own key tiles
+        # are cut into pieces of per = c m tiles (c = tile_q / t_kv, whole
+        # query tiles then have whole pieces per c), only non-empty pieces
+        # are workgroups, and per is the smallest such size -- with at most
+        # max_split pieces per tile -- whose workgroups fit one round of CUs;
+        # kept when that one round of per tiles is shorter than the fixed
+        # ranges' rounds x tiles per split.
+        c = tile_q // t_kv
+        m = max(1, _cdiv(n_kv, c * st.max_split))
+        while True:
+            p_per = c * m
+            pieces = 0
+            for qt in range(n_qt):
+                seen = min(n_kv, _cdiv(min(op.L, (qt + 1) * tile_q), t_kv))
+                pieces += _cdiv(seen, p_per)
+            if heads * pieces <= hw.num_cus or p_per >= n_kv:
+                break
+            m += 1
+        if p_per < _cdiv(grid, hw.num_cus) * per:
+            per = p_per
+            n_split = _cdiv(n_kv, per)
+            grid = heads * pieces
+    rep.update(feasible=True, binding=binding, t_q_wave=t_q, n_waves=n_w, tile_q=tile_q,
+               n_split=n_split, tiles_per_split=per, grid=grid,
                vgpr_est=vgpr_count(hw, atom, op, st, t_q, t_kv, n_w),
                wg_per_cu=grid / hw.num_cus, low_occupancy=grid < hw.num_cus)
     if hw.lds_bytes_per_clk > 0 and hw.mfma_flops_per_clk_cu > 0:

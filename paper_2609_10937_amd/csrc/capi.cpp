@@ -245,8 +245,12 @@ int prepare(const void* Q, const void* K, const void* V, void* O, int B, int H, 
   p.L = L;
   p.n_qt = (L + out->rep.tile_q - 1) / out->rep.tile_q;
   p.n_split = out->rep.n_split;
-  const int n_kv = (L + out->rep.t_kv - 1) / out->rep.t_kv;
-  p.tiles_per_split = (n_kv + out->rep.n_split - 1) / out->rep.n_split;
+  p.tiles_per_split = out->rep.tiles_per_split;
+  p.t_kv = out->rep.t_kv;
+  // Causal pieces: the derivation then reports fewer workgroups than query
+  // tiles times splits (only non-empty pieces).
+  const int64_t n_qt_splits = (int64_t)p.BH * p.n_qt * p.n_split;
+  p.pieces = causal && p.n_split > 1 && out->rep.grid < n_qt_splits ? (int)(out->rep.grid / p.BH) : 0;
   p.causal = causal != 0;
   p.c = scale * 1.4426950408889634f;
   p.tile_q = out->rep.tile_q;

@@ -22,6 +22,9 @@ __device__ __forceinline__ float widen(uint16_t h) {
 // chunks of 256 (row, octet) items of tile t run on XCD t % 8, whose L2 still
 // holds the partials that XCD wrote.  Otherwise one flat order.
 //
+// With causal pieces (FwdParams::pieces) a row has as many slots as its
+// query tile has pieces, computed from the tile sizes.
+//
 // NS is a compile-time bound on the split count (2, 4, 8 or 16).  Every
 // thread first issues all of its loads (NS reference/sum pairs as one 8-byte
 // load each and NS 16-byte partials) and only then does arithmetic, so the
@@ -32,7 +35,7 @@ template <int DT, int D, int NS, bool BY_TILE>
 __global__ void __launch_bounds__(256) combine_kernel(const FwdParams p) {
   using S = typename Mfma<DT>::S;
   constexpr int OCTS = D / 8;
-  const int n_split = p.n_split;
+  int n_split = p.n_split;
   const int64_t rows = (int64_t)p.BH * p.L;
   int64_t row;
   int d8;
@@ -51,6 +54,13 @@ __global__ void __launch_bounds__(256) combine_kernel(const FwdParams p) {
     if (idx >= rows * OCTS) return;
     row = idx / OCTS;
     d8 = (int)(idx - row * OCTS);
+  }
+  if (p.pieces > 0) {
+    // Causal pieces: the row's query tile has one piece per tiles_per_split
+    // of the key tiles it sees; its later slots hold nothing.
+    const int q = (int)(row % p.L), qt = q / p.tile_q;
+    const int seen = (min(p.L, (qt + 1) * p.tile_q) + p.t_kv - 1) / p.t_kv;
+    n_split = (seen + p.tiles_per_split - 1) / p.tiles_per_split;
   }
   const int64_t stride = rows;  // rows per split
   const float2* __restrict__ ml = reinterpret_cast<const float2*>(p.part_ml);
@@ -119,7 +129,7 @@ hipError_t launch_combine(const FwdParams& p, int d, int dtype, hipStream_t s) {
   int xg;
   // Tile order needs whole 256-item chunks per query tile and tiles that
   // cover the sequence.
-  const bool by_tile = fwd_order(p.BH, p.n_qt, p.n_split, &xg) == kOrderTiles && p.tile_q > 0 &&
+  const bool by_tile = fwd_order(p, &xg) == kOrderTiles && p.tile_q > 0 &&
                        (p.tile_q * (d / 8)) % 256 == 0 && (int64_t)p.n_qt * p.tile_q >= p.L;
   const int64_t grid = by_tile ? (int64_t)p.BH * p.n_qt * (p.tile_q * (d / 8) / 256)
                                : ((int64_t)p.BH * p.L * (d / 8) + 255) / 256;

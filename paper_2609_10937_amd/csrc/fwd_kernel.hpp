@@ -370,32 +370,72 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   // head-major, on XCD t % 8), so its L2 fetches the tile's Q rows once
   // instead of once per split: every workgroup loads Q at the start, where
   // its key tiles follow over the whole loop.  Causal launches heavy tiles
-  // (high ranks of the query order) first.  Otherwise the plain order: units
-  // fastest within a rank.
+  // (high ranks of the query order) first; causal with split key ranges
+  // launches only the non-empty pieces of each query tile's own key range
+  // (below).  Otherwise the plain order: units fastest within a rank.
   const int units = p.BH * p.n_split;
   int xg;
-  const FwdOrder order = fwd_order(p.BH, p.n_qt, p.n_split, &xg);
-  int unit, rank;
-  if (order == kOrderUnits) {
-    const int x = blockIdx.x % 8, i = blockIdx.x / 8;
-    const int per_group = xg * p.n_qt;
-    const int gi = i / per_group, r = i - gi * per_group;
-    rank = r / xg;
-    unit = x + 8 * (gi * xg + (r - rank * xg));
-  } else if (order == kOrderTiles) {
-    const int x = blockIdx.x % 8, i = blockIdx.x / 8;
-    const int sp = i % p.n_split;
-    const int t = (i / p.n_split) * 8 + x;
-    const int hd = t / p.n_qt;
-    rank = t - hd * p.n_qt;
-    unit = hd * p.n_split + sp;
-  } else {
-    rank = blockIdx.x / units;
-    unit = blockIdx.x - rank * units;
+  const FwdOrder order = fwd_order(p, &xg);
+  int head = 0, split = 0, qt = 0;
+  bool placed = false;
+  if constexpr (TILE_Q % TKV == 0) {
+    if (order == kOrderPieces) {
+      // Causal with split key ranges: query tile qt sees its first
+      // n_kv(qt) key tiles, cut into pieces of P = tiles_per_split = c m tiles
+      // (c = TILE_Q / TKV).  A whole query tile qt < n_qt - 1 sees c (qt + 1)
+      // tiles, so it has a(qt) = ceil((qt + 1) / m) pieces, and the tiles
+      // below qt have F(qt) = sum_{i=1..qt} ceil(i / m) pieces: with qt = a m + r
+      // (0 <= r < m), F = m a (a + 1) / 2 + r (a + 1).  Heads run fastest; then
+      // the last query tile (whole or not) first, then the whole tiles from the
+      // top, each tile's pieces together.
+      constexpr int C = TILE_Q / TKV;
+      const int P = p.tiles_per_split, m = P / C;
+      head = blockIdx.x % p.BH;
+      const int j = blockIdx.x / p.BH;
+      const int n_last = (min(L, p.n_qt * TILE_Q) + TKV - 1) / TKV;  // key tiles the last query tile sees
+      const int a_last = (n_last + P - 1) / P;
+      if (j < a_last) {
+        qt = p.n_qt - 1;
+        split = j;
+      } else {
+        const int nf = p.n_qt - 1;  // whole query tiles 0 .. nf - 1
+        const int af = nf / m, rf = nf - af * m;
+        const int w_f = m * af * (af + 1) / 2 + rf * (af + 1);
+        const int jp = w_f - 1 - (j - a_last);  // piece index counted from tile 0
+        int a = (int)((__builtin_sqrtf(1.f + 8.f * (float)jp / (float)m) - 1.f) * 0.5f);
+        while (m * (a + 1) * (a + 2) / 2 <= jp) ++a;
+        while (a > 0 && m * a * (a + 1) / 2 > jp) --a;
+        const int rem = jp - m * a * (a + 1) / 2;
+        const int r = rem / (a + 1);
+        qt = a * m + r;
+        split = rem - r * (a + 1);
+      }
+      placed = true;
+    }
   }
-  const int head = unit / p.n_split;
-  const int split = unit - head * p.n_split;
-  const int qt = p.causal ? (p.n_qt - 1 - rank) : rank;
+  if (!placed) {
+    int unit, rank;
+    if (order == kOrderUnits) {
+      const int x = blockIdx.x % 8, i = blockIdx.x / 8;
+      const int per_group = xg * p.n_qt;
+      const int gi = i / per_group, r = i - gi * per_group;
+      rank = r / xg;
+      unit = x + 8 * (gi * xg + (r - rank * xg));
+    } else if (order == kOrderTiles) {
+      const int x = blockIdx.x % 8, i = blockIdx.x / 8;
+      const int sp = i % p.n_split;
+      const int t = (i / p.n_split) * 8 + x;
+      const int hd = t / p.n_qt;
+      rank = t - hd * p.n_qt;
+      unit = hd * p.n_split + sp;
+    } else {
+      rank = blockIdx.x / units;
+      unit = blockIdx.x - rank * units;
+    }
+    head = unit / p.n_split;
+    split = unit - head * p.n_split;
+    qt = p.causal ? (p.n_qt - 1 - rank) : rank;
+  }
 
   const size_t hoff = (size_t)head * (size_t)L * D;
   const uint16_t* __restrict__ Qh = static_cast<const uint16_t*>(p.q) + hoff;

@@ -24,22 +24,30 @@ struct FwdParams {
   int causal;
   float c;              // scale * log2(e): exp(scale*(x - m)) = exp2(c*(x - m))
   int tile_q;           // query rows per workgroup of the fused kernel
+  int t_kv;             // key rows per key tile
+  // Causal with split key ranges: workgroups per head, one per non-empty
+  // piece of tiles_per_split key tiles of a query tile's own key range
+  // (the piece order of fwd_kernel); 0 otherwise.
+  int pieces;
 };
 
 // The fused kernel's workgroup order (the XCD a workgroup runs on is its
 // index mod 8), decided alike on the host and the device:
+//   kOrderPieces  causal with split key ranges: the pieces of each query
+//                 tile's own key range, heaviest query tiles first;
 //   kOrderUnits   units (head, split) spread over the XCDs, xg at a time;
 //   kOrderTiles   with a split key range, all splits of query tile t
 //                 (counted head-major) on XCD t % 8;
 //   kOrderPlain   units fastest within a query rank.
 // xg is the smallest power of two with xg * n_qt >= 64.
-enum FwdOrder { kOrderUnits, kOrderTiles, kOrderPlain };
-__host__ __device__ inline FwdOrder fwd_order(int BH, int n_qt, int n_split, int* xg_out) {
+enum FwdOrder { kOrderPieces, kOrderUnits, kOrderTiles, kOrderPlain };
+__host__ __device__ inline FwdOrder fwd_order(const FwdParams& p, int* xg_out) {
   int xg = 1;
-  while (xg * n_qt < 64) xg *= 2;
+  while (xg * p.n_qt < 64) xg *= 2;
   *xg_out = xg;
-  if ((BH * n_split) % (8 * xg) == 0) return kOrderUnits;
-  if (n_split > 1 && (BH * n_qt) % 8 == 0) return kOrderTiles;
+  if (p.pieces > 0) return kOrderPieces;
+  if ((p.BH * p.n_split) % (8 * xg) == 0) return kOrderUnits;
+  if (p.n_split > 1 && (p.BH * p.n_qt) % 8 == 0) return kOrderTiles;
   return kOrderPlain;
 }
 

@@ -32,6 +32,12 @@ namespace attn {
 
 static int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+static int64_t causal_pieces(int64_t L, int64_t tile_q, int64_t t_kv, int64_t n_qt, int64_t n_kv, int64_t per) {
+  int64_t pieces = 0;
+  for (int64_t qt = 0; qt < n_qt; ++qt) pieces += cdiv(std::min(n_kv, cdiv(std::min(L, (qt + 1) * tile_q), t_kv)), per);
+  return pieces;
+}
+
 int64_t vgpr_estimate(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const attn_op_t* op,
                       int64_t t_q, int64_t t_kv, int64_t n_w) {
   const int64_t lane_words = 4 * (int64_t)hw->wavefront_size;  // bytes in one register across a wave
@@ -153,12 +159,39 @@ int derive_tiles(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const a
     binding = "CU";
   }
 
-  const int64_t grid = heads * n_qt * n_split;
+  const int64_t tile_q = n_w * t_q;
+  int64_t per = cdiv(n_kv, n_split);
+  int64_t grid = heads * n_qt * n_split;
+  if (op->causal && n_split > 1 && tile_q % t_kv == 0) {
+    // Causal: query tile qt sees only its first min(n_kv, ceil(min(L,
+    // (qt+1) tile_q) / t_kv)) key tiles, so fixed key ranges would leave the
+    // early tiles' later splits empty and give the last tiles all the work.
+    // Each query tile's own key tiles are cut into pieces of per = c m tiles
+    // (c = tile_q / t_kv), only non-empty pieces are workgroups, and per is
+    // the smallest such size (at most max_split pieces per tile) whose
+    // workgroups fit one round of CUs.
+    const int64_t c = tile_q / t_kv;
+    int64_t m = std::max<int64_t>(1, cdiv(n_kv, c * op->max_split));
+    int64_t pieces = 0, p_per = 0;
+    for (;; ++m) {
+      p_per = c * m;
+      pieces = causal_pieces(op->L, tile_q, t_kv, n_qt, n_kv, p_per);
+      if (heads * pieces <= hw->num_cus || p_per >= n_kv) break;
+    }
+    // Kept when that one round of p_per tiles is shorter than the fixed
+    // ranges' rounds x tiles per split.
+    if (p_per < cdiv(grid, hw->num_cus) * per) {
+      per = p_per;
+      n_split = cdiv(n_kv, per);
+      grid = heads * pieces;
+    }
+  }
   rep->feasible = 1;
   rep->t_q_wave = (int32_t)t_q;
   rep->n_waves = (int32_t)n_w;
-  rep->tile_q = (int32_t)(n_w * t_q);
+  rep->tile_q = (int32_t)tile_q;
   rep->n_split = (int32_t)n_split;
+  rep->tiles_per_split = (int32_t)per;
   rep->grid = grid;
   rep->vgpr_est = (int32_t)vgpr_estimate(hw, atom, op, t_q, t_kv, n_w);
   rep->wg_per_cu = (double)grid / hw->num_cus;

@@ -65,7 +65,7 @@ def _same(rc, rep, ref):
     assert rep.binding.decode() == ref["binding"]
     if not ref["feasible"]:
         return
-    for k in ("t_kv", "n_waves", "tile_q", "n_split", "grid", "vgpr_est", "vgpr_budget",
+    for k in ("t_kv", "n_waves", "tile_q", "n_split", "tiles_per_split", "grid", "vgpr_est", "vgpr_budget",
               "lds_used", "lds_budget"):
         assert getattr(rep, k) == ref[k], k
     assert rep.t_q_wave == ref["t_q_wave"]
@@ -186,6 +186,26 @@ def test_split_count_by_rounds(shape, split, grid):
     hw = capi.attn_hw_desc_preset("gfx950")
     r = capi.attn_fwd_plan(*shape, 0, capi.ATTN_BF16, hw=hw)
     assert (r.n_split, r.grid, r.binding) == (split, grid, b"CU")
+
+
+@pytest.mark.parametrize("L,per,n_split,grid", [
+    # 64 query tiles of 256 rows, 256 key tiles, 4 key tiles per query tile:
+    # pieces of 4m tiles, m >= ceil(256 / (4 * 16)) = 4.  Query tile qt has
+    # ceil((qt + 1) / m) pieces: m = 9 gives 9 (1 + ... + 7) + 8 = 260 > 256,
+    # m = 10 gives 10 (1 + ... + 6) + 4 * 7 = 238
+    (16384, 40, 7, 238),
+    # 32 query tiles, 128 key tiles, m >= 2: m = 2 gives 2 (1 + ... + 16) =
+    # 272 > 256, m = 3 gives 3 (1 + ... + 10) + 2 * 11 = 187
+    (8192, 12, 11, 187),
+])
+def test_causal_pieces_by_hand(L, per, n_split, grid):
+    """Causal single heads: each query tile's own key tiles are cut into the
+    smallest pieces (whole multiples of the 4 key tiles a query tile adds)
+    whose count fits one round of 256 CUs (worked by hand)."""
+    hw = capi.attn_hw_desc_preset("gfx950")
+    r = capi.attn_fwd_plan(1, 1, L, 128, 1, capi.ATTN_BF16, hw=hw)
+    assert (r.tile_q, r.t_kv) == (256, 64)
+    assert (r.tiles_per_split, r.n_split, r.grid, r.binding) == (per, n_split, grid, b"CU")
 
 
 # ------------------------------------------------------------ argument checks

@@ -173,6 +173,28 @@ EDGE = [(L, d, causal, dt) for L in (1, 17, 100, 1000, 4097) for d in (64, 96, 1
         for causal in (False, True) for dt in ("bf16", "f16")]
 
 
+@pytest.mark.parametrize("L,d,dtype", [(16384, 128, "bf16"), (8192, 128, "f16"), (6000, 128, "bf16"),
+                                       (16384, 64, "bf16"), (16384, 96, "bf16"), (16384, 256, "f16"),
+                                       (9000, 96, "bf16"), (20000, 128, "bf16"), (3000, 256, "bf16")])
+def test_causal_pieces_all_rows(L, d, dtype):
+    """Causal single heads, split as pieces of each query tile's own key range
+    (only non-empty pieces launched, heaviest query tiles first; the merge
+    reads as many slots per row as the row's query tile has pieces): all rows
+    against the oracle."""
+    dt = capi.ATTN_BF16 if dtype == "bf16" else capi.ATTN_F16
+    plan = capi.attn_fwd_plan(1, 1, L, d, True, dt)
+    n_qt = -(-L // plan.tile_q)
+    assert plan.n_split > 1 and plan.tile_q % plan.t_kv == 0 and plan.grid < n_qt * plan.n_split
+    print(f"case causal pieces L{L} d{d} {dtype}: {plan.tiles_per_split} key tiles per piece, "
+          f"{plan.n_split} slots, {plan.grid} workgroups", flush=True)
+    q, k, v = inputs.make_qkv(1, 1, L, d, dtype, seed=3 * L + d)
+    scale = inputs.softmax_scale(d)
+    o = _gpu.fused(_gpu.upload(q, dtype), _gpu.upload(k, dtype), _gpu.upload(v, dtype), scale, True)
+    ref = A.attention(_f64(q, dtype), _f64(k, dtype), _f64(v, dtype), scale, True)
+    mx, mn = _gpu.assert_close(_gpu.download(o, dtype), ref, dtype, f"causal pieces L{L} d{d}")
+    print(f"  max_abs {mx:.3e} mean_abs {mn:.3e}", flush=True)
+
+
 @pytest.mark.parametrize("L,d,causal,dtype", [(10000, 128, False, "bf16"), (10000, 128, True, "f16"),
                                                (9000, 96, False, "bf16")])
 def test_split_counts_not_powers_of_two(L, d, causal, dtype):

@@ -135,9 +135,26 @@ def test_budgets_alignment_maximality(hw, atom, op, st):
                             st.waves_per_wg) > rep["vgpr_budget"]
     assert rep["tile_q"] == rep["n_waves"] * rep["t_q_wave"]
     n_qt = -(-op.L // rep["tile_q"])
-    assert rep["grid"] == op.B * op.H * n_qt * rep["n_split"]
+    n_kv = -(-op.L // rep["t_kv"])
+    per = rep["tiles_per_split"]
     assert 1 <= rep["n_split"] <= max(1, st.max_split)
+    assert rep["n_split"] == -(-n_kv // per)
     assert rep["low_occupancy"] == (rep["grid"] < hw.num_cus)
+    if op.causal and rep["grid"] < op.B * op.H * n_qt * rep["n_split"]:
+        # causal pieces: the grid counts the non-empty pieces of every query
+        # tile's own key range, fits one round, and one key tile less per
+        # piece (keeping whole query tiles in whole pieces) would not
+        c = rep["tile_q"] // rep["t_kv"]
+        assert per % c == 0
+        def pieces(pp):
+            return sum(-(-min(n_kv, -(-min(op.L, (qt + 1) * rep["tile_q"]) // rep["t_kv"])) // pp)
+                       for qt in range(n_qt))
+        assert rep["grid"] == op.B * op.H * pieces(per) <= hw.num_cus
+        if per > c and -(-n_kv // (per - c)) <= st.max_split:
+            assert op.B * op.H * pieces(per - c) > hw.num_cus
+    else:
+        assert rep["grid"] == op.B * op.H * n_qt * rep["n_split"]
+        assert per == -(-n_kv // rep["n_split"])
 
 
 @settings(max_examples=200, deadline=None)
