@@ -166,16 +166,30 @@ def cpu_baseline(w, q, k, v):
                      "sample": f"the same oracle in float64, {n64} passes, {dt64:.2f} s"}}
 
 
-def kernel_source_hash():
-    """Hash of the fused kernel's sources: a traffic figure measured on other sources is stale."""
+def _code_only(text):
+    """C/C++ source without comments and with whitespace runs collapsed: a
+    change to comments alone leaves the code, and its measured traffic, the same."""
+    import re
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
+def _sources_hash(pick):
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2609_10937_amd", "csrc")
     for name in sorted(os.listdir(csrc)):
-        if name.startswith("fwd_") or name == "internal.h":
-            with open(os.path.join(csrc, name), "rb") as f:
-                h.update(name.encode() + f.read())
+        if pick(name):
+            with open(os.path.join(csrc, name), encoding="utf-8") as f:
+                h.update(name.encode() + _code_only(f.read()).encode())
     return h.hexdigest()[:16]
+
+
+def kernel_source_hash():
+    """Hash of the fused kernel's code (comments aside): a traffic figure measured
+    on other code is stale."""
+    return _sources_hash(lambda name: name.startswith("fwd_") or name == "internal.h")
 
 
 def measured_traffic(workload):
@@ -194,15 +208,8 @@ def measured_traffic(workload):
 
 
 def unfused_source_hash():
-    """Hash of the unfused baseline's sources (its products, row softmax and driver)."""
-    import hashlib
-    h = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_2609_10937_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
-        if name.startswith("gemm_") or name in ("softmax.hip", "unfused.hip"):
-            with open(os.path.join(csrc, name), "rb") as f:
-                h.update(name.encode() + f.read())
-    return h.hexdigest()[:16]
+    """Hash of the unfused baseline's code (its products, row softmax and driver)."""
+    return _sources_hash(lambda name: name.startswith("gemm_") or name in ("softmax.hip", "unfused.hip"))
 
 
 def measured_unfused_bytes(workload):

@@ -1,5 +1,7 @@
 // Fused attention forward for gfx950 (CDNA4), one workgroup per
-// (query tile, head, key-range split); Figure 2 of the paper.
+// (query tile, head, key-range split) -- with causal masking and split key
+// ranges, per non-empty piece of a query tile's own key range; Figure 2 of
+// the paper.
 //
 // Each wave owns 16*QB query rows and runs Algorithm 1 over the key/value
 // tiles of its workgroup's range:
@@ -28,9 +30,10 @@
 // LDS holds a ring of ST stages, each a K tile and a V tile stored row-major
 // ([t_kv][d]) in 16-byte chunks, XOR-swizzled per row so that the operand
 // reads of a 16-lane group touch distinct banks.  Tiles move HBM -> LDS with
-// global_load_lds_dwordx4 (lane l of a wave writes bytes 16l..16l+15 of a
-// 1 KB block; each lane picks the source chunk that belongs at its slot), so
-// no registers stage them and nothing is transposed on the way.
+// buffer_load_dwordx4 ... lds through a buffer descriptor per tile (lane l of
+// a wave writes bytes 16l..16l+15 of a 1 KB block; each lane picks the source
+// chunk that belongs at its slot), so no registers stage them and nothing is
+// transposed on the way.
 //
 // Schedule.  A step of a wave is a matrix phase (GEMM2 of the previous tile
 // and GEMM1 of the current one: 64 products plus 4 for the row sums) and a
