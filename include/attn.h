@@ -194,6 +194,11 @@ int attn_fwd(const void* Q, const void* K, const void* V, void* O,
  * reference point (scale*log2(e) times a logit at or below the row's
  * maximum; -inf for a row that saw none of the split's keys) and its sum;
  * attn_fwd_merge weighs the splits with the associative merge and writes O.
+ * A causal plan (attn_fwd_plan) whose grid is below B*H * query tiles *
+ * n_split has cut each query tile's own key tiles into pieces of
+ * tiles_per_split and launches only the non-empty ones: slot k of a row is
+ * then written only when the row's query tile has more than k pieces, and
+ * attn_fwd_merge reads no other slot.
  * The normalised partials add one rounding to the input type before the
  * merge: |O - exact| <= 2u max|V| + fp32 terms (u = 2^-9 bf16, 2^-12 f16).
  * Without a split the required workspace is 0 bytes, attn_fwd_partial writes
