@@ -165,7 +165,8 @@ __global__ void __launch_bounds__(W * 64) softmax_kernel(const SoftmaxParams p) 
       o[e >> 1] = pack2<DT>(exp2_hw(__builtin_fmaf(f[e], kLog2e, -ref)) * inv,
                             exp2_hw(__builtin_fmaf(f[e + 1], kLog2e, -ref)) * inv);
     if constexpr (ALIGNED) {
-      *reinterpret_cast<u32x4_t*>(y + col) = (u32x4_t){o[0], o[1], o[2], o[3]};
+      // The output is not read again here: a streaming (non-temporal) store.
+      __builtin_nontemporal_store((u32x4_t){o[0], o[1], o[2], o[3]}, reinterpret_cast<u32x4_t*>(y + col));
     } else {
 #pragma unroll
       for (int e = 0; e < 8; ++e)
