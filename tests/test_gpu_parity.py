@@ -426,6 +426,27 @@ def test_two_streams_without_synchronisation():
         _gpu.assert_close(_gpu.download(o, dtype), ref, dtype, "two streams")
 
 
+@pytest.mark.parametrize("B,H,L,d,dtype", [(1, 1, 16384, 128, "bf16"), (1, 2, 3000, 256, "f16")])
+def test_partial_then_merge_equals_fused_causal_pieces(B, H, L, d, dtype):
+    """Causal plans that launch pieces of each query tile's own key range: the
+    caller-workspace path (attn_fwd_partial + attn_fwd_merge) equals attn_fwd
+    bit for bit, the merge reading only the slots a row's query tile has."""
+    dt = capi.ATTN_BF16 if dtype == "bf16" else capi.ATTN_F16
+    plan = capi.attn_fwd_plan(B, H, L, d, True, dt)
+    assert plan.grid < B * H * -(-L // plan.tile_q) * plan.n_split
+    print(f"case partial+merge causal pieces B{B} H{H} L{L} d{d} {dtype}", flush=True)
+    q, k, v = (_gpu.upload(x, dtype) for x in inputs.make_qkv(B, H, L, d, dtype, seed=L + 7))
+    scale = inputs.softmax_scale(d)
+    a = _gpu.fused(q, k, v, scale, True)
+    nb = capi.attn_fwd_workspace_bytes(B, H, L, d, True, dt)
+    ws = torch.full((nb,), 0xFF, dtype=torch.uint8, device="cuda")  # unwritten slots hold NaN bits
+    b = torch.empty_like(q)
+    capi.attn_fwd_partial(q, k, v, b, scale, True, ws)
+    capi.attn_fwd_merge(ws, b, scale, True)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
 @pytest.mark.parametrize("name", ["single_head_l16384_d128", "h8_l1024_d128", "tiny_f16_l128_d64"])
 def test_partial_then_merge_equals_fused(name):
     """attn_fwd_partial + attn_fwd_merge with a caller workspace == attn_fwd, bit for bit."""
