@@ -301,6 +301,7 @@ def main():
     ap.add_argument("--no-d256", action="store_true", help="skip the head-dimension-256 workloads")
     ap.add_argument("--no-d96", action="store_true", help="skip the head-dimension-96 workloads")
     ap.add_argument("--no-d64", action="store_true", help="skip the head-dimension-64 workloads")
+    ap.add_argument("--no-causal-few", action="store_true", help="skip the few-head causal workloads")
     ap.add_argument("--no-softmax", action="store_true", help="skip the row-softmax operator")
     ap.add_argument("--no-gemm", action="store_true", help="skip the GEMM operator")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -474,7 +475,8 @@ def main():
                         "tflops": round(flops(w3) / (ev3 * 1e-3) / 1e12, 1),
                         "pct_peak": round(100 * flops(w3) / (ev3 * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 1),
                         "tiles": {"t_kv": p3.t_kv, "t_q_wave": p3.t_q_wave, "n_waves": p3.n_waves,
-                                  "n_split": p3.n_split, "grid": p3.grid}})
+                                  "n_split": p3.n_split, "tiles_per_split": p3.tiles_per_split,
+                                  "grid": p3.grid}})
             del t3, o3
             torch.cuda.empty_cache()
         return out
@@ -482,6 +484,7 @@ def main():
     d256 = None if args.no_d256 else head_dim_leg(inputs.HEAD_DIM_256)
     d96 = None if args.no_d96 else head_dim_leg(inputs.HEAD_DIM_96)
     d64 = None if args.no_d64 else head_dim_leg(inputs.HEAD_DIM_64)
+    causal_few = None if args.no_causal_few else head_dim_leg(inputs.CAUSAL_FEW_HEADS)
 
     smx = None
     if not args.no_softmax:
@@ -614,6 +617,7 @@ def main():
         "head_dim_256": d256,
         "head_dim_96": d96,
         "head_dim_64": d64,
+        "causal_few_heads": causal_few,
         "softmax": smx,
         "gemm": gemm,
         "cpu_baseline": cpu,

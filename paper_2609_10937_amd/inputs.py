@@ -86,6 +86,14 @@ HEAD_DIM_64 = (
 )
 WORKLOADS.update({w.name: w for w in HEAD_DIM_64})
 
+# Causal attention with few heads, whose key split runs as pieces of each query
+# tile's own key range: one head and two heads at L = 16384.
+CAUSAL_FEW_HEADS = (
+    Workload("causal_single_head_l16384_d128", 1, 1, 16384, 128, "bf16", True, 1.0, 1231),
+    Workload("causal_h2_l16384_d128", 1, 2, 16384, 128, "bf16", True, 1.0, 1232),
+)
+WORKLOADS.update({w.name: w for w in CAUSAL_FEW_HEADS})
+
 
 def softmax_scale(d: int) -> float:
     """1/sqrt(d) evaluated in float32, returned as the Python float of that value."""
