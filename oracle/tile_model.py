@@ -202,6 +202,23 @@ def derive(hw, atom, op, st):
             per = p_per
             n_split = _cdiv(n_kv, per)
             grid = heads * pieces
+    elif (op.causal and n_split == 1 and tile_q % t_kv == 0 and st.max_split >= 2
+          and hw.num_cus <= heads * n_qt < 2 * hw.num_cus):
+        # Causal launches that fill between one and two rounds unsplit are
+        # bound by their longest query tile (n_kv key tiles against an average
+        # of about half that per CU).  Halves of a query tile's own key range
+        # (whole multiples of c key tiles), when the halves fit two rounds of
+        # CUs and a half is at least 32 key tiles: four times the measured
+        # fixed cost of a workgroup, about 8 steps.
+        c = tile_q // t_kv
+        half = c * _cdiv(_cdiv(n_kv, 2), c)
+        halves = heads * sum(_cdiv(min(n_kv, _cdiv(min(op.L, (qt + 1) * tile_q), t_kv)), half)
+                             for qt in range(n_qt))
+        if 32 <= half < n_kv and halves <= 2 * hw.num_cus:
+            per = half
+            n_split = _cdiv(n_kv, per)
+            grid = halves
+            binding = "CU"
     rep.update(feasible=True, binding=binding, t_q_wave=t_q, n_waves=n_w, tile_q=tile_q,
                n_split=n_split, tiles_per_split=per, grid=grid,
                vgpr_est=vgpr_count(hw, atom, op, st, t_q, t_kv, n_w),

@@ -383,14 +383,17 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   bool placed = false;
   if constexpr (TILE_Q % TKV == 0) {
     if (order == kOrderPieces) {
-      // Causal with split key ranges: query tile qt sees its first
-      // n_kv(qt) key tiles, cut into pieces of P = tiles_per_split = c m tiles
-      // (c = TILE_Q / TKV).  A whole query tile qt < n_qt - 1 sees c (qt + 1)
-      // tiles, so it has a(qt) = ceil((qt + 1) / m) pieces, and the tiles
-      // below qt have F(qt) = sum_{i=1..qt} ceil(i / m) pieces: with qt = a m + r
-      // (0 <= r < m), F = m a (a + 1) / 2 + r (a + 1).  Heads run fastest; then
-      // the last query tile (whole or not) first, then the whole tiles from the
-      // top, each tile's pieces together.
+      // Causal with split key ranges: query tile qt sees its first n_kv(qt)
+      // key tiles, cut into pieces of P = tiles_per_split = C m tiles
+      // (C = TILE_Q / TKV); a whole query tile qt < n_qt - 1 sees C (qt + 1)
+      // tiles and so has ceil((qt + 1) / m) pieces.  Heads run fastest; then
+      // the last query tile's pieces (whole tile or not); then, piece-major,
+      // the first piece of every whole tile (heaviest first), then every
+      // second piece, ...: piece k exists for the nf - k m whole tiles
+      // qt >= k m (nf = n_qt - 1), so pieces 0 .. k-1 take
+      // G(k) = k nf - m k (k - 1) / 2 places.  Consecutive workgroups go to
+      // consecutive XCDs, and this order gives each XCD a like mix of long
+      // and short pieces.
       constexpr int C = TILE_Q / TKV;
       const int P = p.tiles_per_split, m = P / C;
       head = blockIdx.x % p.BH;
@@ -401,17 +404,16 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
         qt = p.n_qt - 1;
         split = j;
       } else {
-        const int nf = p.n_qt - 1;  // whole query tiles 0 .. nf - 1
-        const int af = nf / m, rf = nf - af * m;
-        const int w_f = m * af * (af + 1) / 2 + rf * (af + 1);
-        const int jp = w_f - 1 - (j - a_last);  // piece index counted from tile 0
-        int a = (int)((__builtin_sqrtf(1.f + 8.f * (float)jp / (float)m) - 1.f) * 0.5f);
-        while (m * (a + 1) * (a + 2) / 2 <= jp) ++a;
-        while (a > 0 && m * a * (a + 1) / 2 > jp) --a;
-        const int rem = jp - m * a * (a + 1) / 2;
-        const int r = rem / (a + 1);
-        qt = a * m + r;
-        split = rem - r * (a + 1);
+        const int jp = j - a_last, nf = p.n_qt - 1;
+        const int K = (nf + m - 1) / m;  // pieces of the longest whole tile
+        const float hb = (float)nf + 0.5f * (float)m;
+        const float disc = fmaxf(0.f, hb * hb - 2.f * (float)m * (float)jp);
+        int k = (int)((hb - __builtin_sqrtf(disc)) / (float)m);
+        k = min(max(k, 0), K - 1);
+        while (k + 1 < K && (k + 1) * nf - m * (k + 1) * k / 2 <= jp) ++k;
+        while (k > 0 && k * nf - m * k * (k - 1) / 2 > jp) --k;
+        qt = nf - 1 - (jp - (k * nf - m * k * (k - 1) / 2));
+        split = k;
       }
       placed = true;
     }

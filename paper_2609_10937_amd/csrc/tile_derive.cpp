@@ -185,6 +185,23 @@ int derive_tiles(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const a
       n_split = cdiv(n_kv, per);
       grid = heads * pieces;
     }
+  } else if (op->causal && n_split == 1 && tile_q % t_kv == 0 && op->max_split >= 2 &&
+             heads * n_qt >= hw->num_cus && heads * n_qt < 2 * (int64_t)hw->num_cus) {
+    // Causal launches that fill between one and two rounds unsplit are bound
+    // by their longest query tile (n_kv key tiles against an average of about
+    // half that per CU).  Halves of a query tile's own key range (whole
+    // multiples of c key tiles), when the halves fit two rounds of CUs and a
+    // half is at least 32 key tiles: four times the measured fixed cost of a
+    // workgroup, about 8 steps.
+    const int64_t c = tile_q / t_kv;
+    const int64_t half = c * cdiv(cdiv(n_kv, 2), c);
+    const int64_t halves = heads * causal_pieces(op->L, tile_q, t_kv, n_qt, n_kv, half);
+    if (half >= 32 && half < n_kv && halves <= 2 * (int64_t)hw->num_cus) {
+      per = half;
+      n_split = cdiv(n_kv, per);
+      grid = halves;
+      binding = "CU";
+    }
   }
   rep->feasible = 1;
   rep->t_q_wave = (int32_t)t_q;

@@ -208,6 +208,23 @@ def test_causal_pieces_by_hand(L, per, n_split, grid):
     assert (r.tiles_per_split, r.n_split, r.grid, r.binding) == (per, n_split, grid, b"CU")
 
 
+def test_causal_halves_over_two_rounds_by_hand():
+    """Four causal heads at L = 16384 fill one round of 256 CUs unsplit (64
+    query tiles each), bound by the last tiles' 256 key tiles.  Halves of 128
+    key tiles: query tiles 32 .. 63 (more than 128 key tiles) have two pieces,
+    0 .. 31 one, so 4 (2 * 32 + 32) = 384 workgroups over two rounds."""
+    hw = capi.attn_hw_desc_preset("gfx950")
+    r = capi.attn_fwd_plan(1, 4, 16384, 128, 1, capi.ATTN_BF16, hw=hw)
+    assert (r.tile_q, r.t_kv, r.tiles_per_split, r.n_split, r.grid, r.binding) == (256, 64, 128, 2, 384, b"CU")
+    # 32 heads at L = 2048: halves would be 16 key tiles, too short to pay; unsplit
+    r = capi.attn_fwd_plan(1, 32, 2048, 128, 1, capi.ATTN_BF16, hw=hw)
+    assert (r.n_split, r.grid) == (1, 256)
+    # 6 heads at L = 16384: 384 query tiles unsplit; halves would be 6 * 96 =
+    # 576 workgroups, more than two rounds; unsplit
+    r = capi.attn_fwd_plan(1, 6, 16384, 128, 1, capi.ATTN_BF16, hw=hw)
+    assert (r.n_split, r.grid) == (1, 384)
+
+
 # ------------------------------------------------------------ argument checks
 
 P = 1 << 20  # a 16-byte aligned fake device address; never dereferenced

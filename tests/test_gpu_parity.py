@@ -195,6 +195,24 @@ def test_causal_pieces_all_rows(L, d, dtype):
     print(f"  max_abs {mx:.3e} mean_abs {mn:.3e}", flush=True)
 
 
+@pytest.mark.parametrize("H,L,d,dtype", [(16, 4096, 128, "bf16"), (8, 8192, 128, "f16"), (4, 16384, 64, "bf16")])
+def test_causal_halves_all_rows(H, L, d, dtype):
+    """Causal launches that fill one round of CUs unsplit, run as halves of each
+    query tile's own key range over two rounds (piece-major order): all rows
+    of every head against the oracle."""
+    dt = capi.ATTN_BF16 if dtype == "bf16" else capi.ATTN_F16
+    plan = capi.attn_fwd_plan(1, H, L, d, True, dt)
+    n_qt = -(-L // plan.tile_q)
+    assert plan.n_split == 2 and 256 < plan.grid < H * n_qt * 2
+    print(f"case causal halves H{H} L{L} d{d} {dtype}: {plan.grid} workgroups", flush=True)
+    q, k, v = inputs.make_qkv(1, H, L, d, dtype, seed=5 * L + H)
+    scale = inputs.softmax_scale(d)
+    o = _gpu.fused(_gpu.upload(q, dtype), _gpu.upload(k, dtype), _gpu.upload(v, dtype), scale, True)
+    ref = A.attention(_f64(q, dtype), _f64(k, dtype), _f64(v, dtype), scale, True)
+    mx, mn = _gpu.assert_close(_gpu.download(o, dtype), ref, dtype, f"causal halves H{H} L{L} d{d}")
+    print(f"  max_abs {mx:.3e} mean_abs {mn:.3e}", flush=True)
+
+
 @pytest.mark.parametrize("L,d,causal,dtype", [(10000, 128, False, "bf16"), (10000, 128, True, "f16"),
                                                (9000, 96, False, "bf16")])
 def test_split_counts_not_powers_of_two(L, d, causal, dtype):

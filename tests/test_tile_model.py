@@ -149,9 +149,19 @@ def test_budgets_alignment_maximality(hw, atom, op, st):
         def pieces(pp):
             return sum(-(-min(n_kv, -(-min(op.L, (qt + 1) * rep["tile_q"]) // rep["t_kv"])) // pp)
                        for qt in range(n_qt))
-        assert rep["grid"] == op.B * op.H * pieces(per) <= hw.num_cus
-        if per > c and -(-n_kv // (per - c)) <= st.max_split:
-            assert op.B * op.H * pieces(per - c) > hw.num_cus
+        heads = op.B * op.H
+        assert rep["grid"] == heads * pieces(per)
+        if heads * n_qt < hw.num_cus:
+            # one round, and one step of c key tiles less per piece would not fit it
+            assert rep["grid"] <= hw.num_cus
+            if per > c and -(-n_kv // (per - c)) <= st.max_split:
+                assert heads * pieces(per - c) > hw.num_cus
+        else:
+            # filled between one and two rounds unsplit: halves of at least 32
+            # key tiles that fit two rounds
+            assert heads * n_qt < 2 * hw.num_cus and rep["n_split"] == 2
+            assert per == c * -(-(-(-n_kv // 2)) // c) and 32 <= per < n_kv
+            assert rep["grid"] <= 2 * hw.num_cus
     else:
         assert rep["grid"] == op.B * op.H * n_qt * rep["n_split"]
         assert per == -(-n_kv // rep["n_split"])
