@@ -103,6 +103,9 @@ typedef struct {
   int32_t vgpr_fixed;           /* registers per lane outside the counted arrays: lane addresses,
                                    copy offsets, constants (the paper's instance: 16) */
   int32_t max_split;            /* key-range splits the CU rule may use (1 = none) */
+  int32_t wg_fixed_steps;       /* fixed cost of one workgroup (prologue, epilogue) in steps of one
+                                   key tile, which the CU rule weighs against the tiles per split
+                                   (0 = none) */
 } attn_op_t;
 
 /* Result of the derivation (Section 4: tiles, feasibility, binding constraint). */

@@ -77,6 +77,7 @@ class Structure:
     waves_per_simd: int = 1  # resident waves per SIMD (divides the register file)
     vgpr_fixed: int = 16     # addresses, loop state, constants
     max_split: int = 1       # key-range splits allowed by the CU rule
+    wg_fixed_steps: int = 0  # a workgroup's fixed cost in steps of one key tile (CU rule)
 
 
 def _cdiv(a, b):
@@ -144,15 +145,17 @@ def derive(hw, atom, op, st):
     fills = False
     if heads * n_qt < hw.num_cus and st.max_split > 1:
         # Split count (our addition to the CU rule): the grid runs in rounds of
-        # num_cus workgroups and a workgroup's time follows its key tiles, so
-        # take the count with the fewest rounds x tiles per split (the smallest
-        # on ties).  Counts that leave a split empty collapse onto a smaller one.
+        # num_cus workgroups and a workgroup's time is its fixed cost plus its
+        # key tiles, so take the count with the fewest rounds x (fixed cost +
+        # tiles per split), the smallest on ties.  Counts that leave a split
+        # empty collapse onto a smaller one.
         s_max = _cdiv(n_kv, _cdiv(n_kv, min(st.max_split, n_kv)))
         best = None
         for s in range(1, s_max + 1):
             per = _cdiv(n_kv, s)
             eff = _cdiv(n_kv, per)
-            cost = _cdiv(heads * n_qt * eff, hw.num_cus) * per
+            # rounds x (a workgroup's fixed cost + its key tiles)
+            cost = _cdiv(heads * n_qt * eff, hw.num_cus) * (st.wg_fixed_steps + per)
             if best is None or cost < best[0]:
                 best = (cost, eff)
         fills = heads * n_qt * s_max >= hw.num_cus
@@ -185,8 +188,8 @@ def derive(hw, atom, op, st):
         # query tiles then have whole pieces per c), only non-empty pieces
         # are workgroups, and per is the smallest such size -- with at most
         # max_split pieces per tile -- whose workgroups fit one round of CUs;
-        # kept when that one round of per tiles is shorter than the fixed
-        # ranges' rounds x tiles per split.
+        # kept when that one round is shorter than the fixed ranges' rounds,
+        # each workgroup costing its fixed cost plus its key tiles.
         c = tile_q // t_kv
         m = max(1, _cdiv(n_kv, c * st.max_split))
         while True:
@@ -198,7 +201,8 @@ def derive(hw, atom, op, st):
             if heads * pieces <= hw.num_cus or p_per >= n_kv:
                 break
             m += 1
-        if p_per < _cdiv(grid, hw.num_cus) * per:
+        c0 = st.wg_fixed_steps
+        if c0 + p_per < _cdiv(grid, hw.num_cus) * (c0 + per):
             per = p_per
             n_split = _cdiv(n_kv, per)
             grid = heads * pieces
@@ -208,13 +212,12 @@ def derive(hw, atom, op, st):
         # bound by their longest query tile (n_kv key tiles against an average
         # of about half that per CU).  Halves of a query tile's own key range
         # (whole multiples of c key tiles), when the halves fit two rounds of
-        # CUs and a half is at least 32 key tiles: four times the measured
-        # fixed cost of a workgroup, about 8 steps.
+        # CUs and a half is at least four times a workgroup's fixed cost.
         c = tile_q // t_kv
         half = c * _cdiv(_cdiv(n_kv, 2), c)
         halves = heads * sum(_cdiv(min(n_kv, _cdiv(min(op.L, (qt + 1) * tile_q), t_kv)), half)
                              for qt in range(n_qt))
-        if 32 <= half < n_kv and halves <= 2 * hw.num_cus:
+        if 4 * st.wg_fixed_steps <= half < n_kv and halves <= 2 * hw.num_cus:
             per = half
             n_split = _cdiv(n_kv, per)
             grid = halves

@@ -72,7 +72,7 @@ class Op(_Struct):
                 ("kv_lds_den", c_int32), ("kv_tiles", c_int32), ("stage_tiles", c_int32), ("score_tiles", c_int32),
                 ("p_tiles", c_int32), ("stat_regs", c_int32), ("operand_frags", c_int32),
                 ("waves_per_wg", c_int32), ("waves_per_simd", c_int32), ("vgpr_fixed", c_int32),
-                ("max_split", c_int32)]
+                ("max_split", c_int32), ("wg_fixed_steps", c_int32)]
 
 
 class TileReport(_Struct):

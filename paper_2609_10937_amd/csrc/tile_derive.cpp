@@ -68,7 +68,7 @@ int derive_tiles(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const a
   if (op->B <= 0 || op->H <= 0 || op->L <= 0 || op->d <= 0 || op->elem_bytes <= 0) return ATTN_E_ARG;
   if (op->kv_lds_num <= 0 || op->kv_lds_den <= 0 || op->kv_tiles <= 0 || op->stage_tiles < 0 || op->score_tiles < 1 ||
       op->p_tiles < 0 || op->stat_regs < 0 || op->operand_frags < 0 || op->waves_per_wg <= 0 ||
-      op->waves_per_simd <= 0 || op->vgpr_fixed < 0 || op->max_split < 1)
+      op->waves_per_simd <= 0 || op->vgpr_fixed < 0 || op->max_split < 1 || op->wg_fixed_steps < 0)
     return ATTN_E_ARG;
 
   memset(rep, 0, sizeof(*rep));
@@ -133,14 +133,15 @@ int derive_tiles(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const a
   bool fills = false;
   if (heads * n_qt < hw->num_cus && op->max_split > 1) {
     // The grid runs in rounds of num_cus workgroups and a workgroup's time
-    // follows its key tiles: take the split count with the fewest rounds x
-    // tiles per split, the smallest on ties; a count that would leave a split
-    // empty collapses onto the smaller count with the same tiles per split.
+    // is its fixed cost plus its key tiles: take the split count with the
+    // fewest rounds x (wg_fixed_steps + tiles per split), the smallest on
+    // ties; a count that would leave a split empty collapses onto the smaller
+    // count with the same tiles per split.
     const int64_t s_max = cdiv(n_kv, cdiv(n_kv, std::min((int64_t)op->max_split, n_kv)));
     int64_t best_cost = -1, best = 1;
     for (int64_t s = 1; s <= s_max; ++s) {
       const int64_t per = cdiv(n_kv, s), eff = cdiv(n_kv, per);
-      const int64_t cost = cdiv(heads * n_qt * eff, hw->num_cus) * per;
+      const int64_t cost = cdiv(heads * n_qt * eff, hw->num_cus) * (op->wg_fixed_steps + per);
       if (best_cost < 0 || cost < best_cost) best_cost = cost, best = eff;
     }
     fills = heads * n_qt * s_max >= hw->num_cus;
@@ -178,9 +179,10 @@ int derive_tiles(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const a
       pieces = causal_pieces(op->L, tile_q, t_kv, n_qt, n_kv, p_per);
       if (heads * pieces <= hw->num_cus || p_per >= n_kv) break;
     }
-    // Kept when that one round of p_per tiles is shorter than the fixed
-    // ranges' rounds x tiles per split.
-    if (p_per < cdiv(grid, hw->num_cus) * per) {
+    // Kept when that one round is shorter than the fixed ranges' rounds, each
+    // workgroup costing wg_fixed_steps plus its key tiles.
+    const int64_t c0 = op->wg_fixed_steps;
+    if (c0 + p_per < cdiv(grid, hw->num_cus) * (c0 + per)) {
       per = p_per;
       n_split = cdiv(n_kv, per);
       grid = heads * pieces;
@@ -191,12 +193,11 @@ int derive_tiles(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const a
     // by their longest query tile (n_kv key tiles against an average of about
     // half that per CU).  Halves of a query tile's own key range (whole
     // multiples of c key tiles), when the halves fit two rounds of CUs and a
-    // half is at least 32 key tiles: four times the measured fixed cost of a
-    // workgroup, about 8 steps.
+    // half is at least four times a workgroup's fixed cost.
     const int64_t c = tile_q / t_kv;
     const int64_t half = c * cdiv(cdiv(n_kv, 2), c);
     const int64_t halves = heads * causal_pieces(op->L, tile_q, t_kv, n_qt, n_kv, half);
-    if (half >= 32 && half < n_kv && halves <= 2 * (int64_t)hw->num_cus) {
+    if (half >= 4 * (int64_t)op->wg_fixed_steps && half < n_kv && halves <= 2 * (int64_t)hw->num_cus) {
       per = half;
       n_split = cdiv(n_kv, per);
       grid = halves;

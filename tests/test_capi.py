@@ -56,7 +56,8 @@ def _to_c(hw, atom, op, st):
                 kv_lds_num=st.kv_lds_num, kv_lds_den=st.kv_lds_den, kv_tiles=st.kv_tiles,
                 stage_tiles=st.stage_tiles, score_tiles=st.score_tiles, p_tiles=st.p_tiles,
                 stat_regs=st.stat_regs, operand_frags=st.operand_frags, waves_per_wg=st.waves_per_wg,
-                waves_per_simd=st.waves_per_simd, vgpr_fixed=st.vgpr_fixed, max_split=st.max_split)
+                waves_per_simd=st.waves_per_simd, vgpr_fixed=st.vgpr_fixed, max_split=st.max_split,
+                wg_fixed_steps=st.wg_fixed_steps)
     return h, a, o
 
 
@@ -113,7 +114,8 @@ st_s = stg.builds(T.Structure, kv_lds_num=stg.just(1), kv_lds_den=stg.sampled_fr
                   stat_regs=stg.integers(0, 8), operand_frags=stg.integers(0, 8),
                   waves_per_wg=stg.sampled_from([1, 2, 4, 8, 16]),
                   waves_per_simd=stg.sampled_from([1, 2, 4]),
-                  vgpr_fixed=stg.integers(0, 128), max_split=stg.sampled_from([1, 2, 8, 16]))
+                  vgpr_fixed=stg.integers(0, 128), max_split=stg.sampled_from([1, 2, 8, 16]),
+                  wg_fixed_steps=stg.sampled_from([0, 1, 8, 20]))
 
 
 @settings(max_examples=1500, deadline=None)
@@ -167,22 +169,24 @@ def test_headline_plans():
 
 
 @pytest.mark.parametrize("shape,split,grid", [
-    # 64 query tiles, 256 key tiles: 4 splits fill one round exactly (8 tie at
-    # two rounds of 32 tiles; the smaller count wins)
+    # Cost: rounds x (8 steps of fixed cost + key tiles per split).
+    # 64 query tiles, 256 key tiles: 4 splits fill one round exactly,
+    # 8 + 64 = 72 (8 splits: two rounds of 8 + 32 = 80)
     ((1, 1, 16384, 128), 4, 256),
-    # d = 96: 43 query tiles of 384 rows, 256 key tiles.  8 splits: 344
-    # workgroups, two rounds of 32 tiles = 64; 5 splits: one round of 52;
-    # 11 splits: two rounds of 24 = 48, the fewest
-    ((1, 1, 16384, 96), 11, 473),
+    # d = 96: 43 query tiles of 384 rows, 256 key tiles.  5 splits: one round
+    # of 215 workgroups, 8 + 52 = 60; 11 splits: two rounds of 8 + 24 = 64;
+    # 8 splits: two rounds of 8 + 32 = 80
+    ((1, 1, 16384, 96), 5, 215),
     # L = 10000: 40 query tiles, 157 key tiles; 6 splits of 27 tiles make one
-    # round of 240 (8 splits: 320 workgroups, two rounds of 20 = 40)
+    # round of 240, 8 + 27 = 35 (8 splits: 320 workgroups, two rounds of
+    # 8 + 20 = 56)
     ((1, 1, 10000, 128), 6, 240),
     # splitting cannot fill the CUs: the most splits (16), then halve the waves
     ((1, 4, 1000, 96), 16, 384),
 ])
 def test_split_count_by_rounds(shape, split, grid):
-    """The split count minimises rounds of CU-count workgroups times key tiles
-    per split (worked by hand in each case)."""
+    """The split count minimises rounds of CU-count workgroups times (a
+    workgroup's fixed cost of 8 steps + key tiles per split), worked by hand."""
     hw = capi.attn_hw_desc_preset("gfx950")
     r = capi.attn_fwd_plan(*shape, 0, capi.ATTN_BF16, hw=hw)
     assert (r.n_split, r.grid, r.binding) == (split, grid, b"CU")

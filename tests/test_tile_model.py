@@ -114,7 +114,8 @@ st_s = stg.builds(T.Structure, kv_lds_num=stg.just(1), kv_lds_den=stg.sampled_fr
                   score_tiles=stg.sampled_from([1, 2]), p_tiles=stg.sampled_from([0, 1]),
                   stat_regs=stg.integers(0, 8), operand_frags=stg.integers(0, 6),
                   waves_per_wg=stg.sampled_from([1, 2, 4, 8]), waves_per_simd=stg.sampled_from([1, 2]),
-                  vgpr_fixed=stg.integers(0, 64), max_split=stg.sampled_from([1, 4, 8, 16]))
+                  vgpr_fixed=stg.integers(0, 64), max_split=stg.sampled_from([1, 4, 8, 16]),
+                  wg_fixed_steps=stg.sampled_from([0, 8]))
 
 
 @settings(max_examples=400, deadline=None)
@@ -160,7 +161,7 @@ def test_budgets_alignment_maximality(hw, atom, op, st):
             # filled between one and two rounds unsplit: halves of at least 32
             # key tiles that fit two rounds
             assert heads * n_qt < 2 * hw.num_cus and rep["n_split"] == 2
-            assert per == c * -(-(-(-n_kv // 2)) // c) and 32 <= per < n_kv
+            assert per == c * -(-(-(-n_kv // 2)) // c) and 4 * st.wg_fixed_steps <= per < n_kv
             assert rep["grid"] <= 2 * hw.num_cus
     else:
         assert rep["grid"] == op.B * op.H * n_qt * rep["n_split"]

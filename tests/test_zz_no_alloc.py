@@ -48,14 +48,15 @@ def test_noalloc_without_split_and_refusal():
     print(f"case noalloc {w.name} (no split)", flush=True)
     _, a, b = _run_both(w)
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
-    big = inputs.WORKLOADS["single_head_l16384_d96"]  # 11 splits: 34.4 MiB of partials
-    nb = capi.attn_fwd_workspace_bytes(big.B, big.H, big.L, big.d, big.causal, capi.ATTN_BF16)
+    # one head, L = 20000, d = 96: 9 key splits, 36.0 MB of partials
+    B, H, L, d = 1, 1, 20000, 96
+    nb = capi.attn_fwd_workspace_bytes(B, H, L, d, False, capi.ATTN_BF16)
     assert nb > capi.NOALLOC_SCRATCH_BYTES
-    print(f"case noalloc refusal {big.name} workspace {nb} bytes", flush=True)
-    t = torch.zeros((big.B, big.H, big.L, big.d), dtype=torch.bfloat16, device="cuda")
+    print(f"case noalloc refusal B{B} H{H} L{L} d{d} workspace {nb} bytes", flush=True)
+    t = torch.zeros((B, H, L, d), dtype=torch.bfloat16, device="cuda")
     o = torch.zeros_like(t)
     with pytest.raises(capi.AttnError) as e:
-        capi.attn_fwd_noalloc(t, t, t, o, big.scale, big.causal)
+        capi.attn_fwd_noalloc(t, t, t, o, inputs.softmax_scale(d), False)
     assert e.value.status == capi.CODE["ATTN_E_SCRATCH"]
     torch.cuda.synchronize()
     assert not torch.any(o.view(torch.int16))  # refused before any device work
