@@ -225,20 +225,37 @@ def attn_strerror(status: int) -> str:
 
 # ------------------------------------------------------------ device calls
 
-def dtype_code(t) -> int:
+# torch glue, looked up once: the dtype codes and torch's current-stream
+# getter (the raw handle as an integer, without building a Stream object).
+_DTYPES = None
+_RAW_STREAM = None
+
+
+def _torch_glue():
+    global _DTYPES, _RAW_STREAM
     import torch
-    if t.dtype == torch.bfloat16:
-        return ATTN_BF16
-    if t.dtype == torch.float16:
-        return ATTN_F16
-    raise AttnError(CODE["ATTN_E_DTYPE"], f"unsupported tensor dtype {t.dtype}")
+    _RAW_STREAM = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+    _DTYPES = {torch.bfloat16: ATTN_BF16, torch.float16: ATTN_F16}
+    return _DTYPES
+
+
+def dtype_code(t) -> int:
+    code = (_DTYPES or _torch_glue()).get(t.dtype)
+    if code is None:
+        raise AttnError(CODE["ATTN_E_DTYPE"], f"unsupported tensor dtype {t.dtype}")
+    return code
 
 
 def _stream_ptr(t, stream):
-    import torch
+    """The HIP stream handle: `stream`'s, else torch's current stream on t's device."""
     if stream is None:
+        if _DTYPES is None:
+            _torch_glue()
+        if _RAW_STREAM is not None:
+            return _RAW_STREAM(t.get_device())
+        import torch
         stream = torch.cuda.current_stream(t.device)
-    return c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
 
 
 def _dev_ptr(t):
@@ -246,15 +263,20 @@ def _dev_ptr(t):
         raise AttnError(CODE["ATTN_E_ARG"], "tensor must be on the GPU")
     if not t.is_contiguous():
         raise AttnError(CODE["ATTN_E_ARG"], "tensor must be contiguous [B, H, L, d]")
-    return c_void_p(t.data_ptr())
+    return t.data_ptr()
+
+
+def _same(q, k, v, o):
+    shape, dt = q.shape, q.dtype
+    for t in (k, v, o):
+        if t.shape != shape or t.dtype != dt:
+            raise AttnError(CODE["ATTN_E_SHAPE"], "q, k, v, o must share shape and dtype")
 
 
 def attn_fwd(q, k, v, o, scale: float, causal: bool, stream=None):
     """Enqueue the fused forward on `stream` (default: torch's current stream)."""
     B, H, L, d = q.shape
-    for t in (k, v, o):
-        if tuple(t.shape) != (B, H, L, d) or t.dtype != q.dtype:
-            raise AttnError(CODE["ATTN_E_SHAPE"], "q, k, v, o must share shape and dtype")
+    _same(q, k, v, o)
     _check(load().attn_fwd(_dev_ptr(q), _dev_ptr(k), _dev_ptr(v), _dev_ptr(o), B, H, L, d,
                            float(scale), int(causal), dtype_code(q), _stream_ptr(q, stream)))
 
@@ -263,9 +285,7 @@ def attn_fwd_noalloc(q, k, v, o, scale: float, causal: bool, stream=None):
     """attn_fwd with the split workspace in the library's static per-GPU array
     (no allocation; calls that overlap on one GPU race on it)."""
     B, H, L, d = q.shape
-    for t in (k, v, o):
-        if tuple(t.shape) != (B, H, L, d) or t.dtype != q.dtype:
-            raise AttnError(CODE["ATTN_E_SHAPE"], "q, k, v, o must share shape and dtype")
+    _same(q, k, v, o)
     _check(load().attn_fwd_noalloc(_dev_ptr(q), _dev_ptr(k), _dev_ptr(v), _dev_ptr(o), B, H, L, d,
                                    float(scale), int(causal), dtype_code(q), _stream_ptr(q, stream)))
 
@@ -284,6 +304,7 @@ def _ws(workspace):
 
 def attn_fwd_partial(q, k, v, o, scale: float, causal: bool, workspace=None, stream=None):
     B, H, L, d = q.shape
+    _same(q, k, v, o)
     ws, nb = _ws(workspace)
     _check(load().attn_fwd_partial(_dev_ptr(q), _dev_ptr(k), _dev_ptr(v), _dev_ptr(o), B, H, L, d, float(scale),
                                    int(causal), dtype_code(q), ws, nb, _stream_ptr(q, stream)))
@@ -298,9 +319,7 @@ def attn_fwd_merge(workspace, o, scale: float, causal: bool, stream=None):
 
 def attn_fwd_unfused(q, k, v, o, scale: float, causal: bool, workspace, stream=None):
     B, H, L, d = q.shape
-    for t in (k, v, o):
-        if tuple(t.shape) != (B, H, L, d) or t.dtype != q.dtype:
-            raise AttnError(CODE["ATTN_E_SHAPE"], "q, k, v, o must share shape and dtype")
+    _same(q, k, v, o)
     nbytes = workspace.numel() * workspace.element_size()
     _check(load().attn_fwd_unfused(_dev_ptr(q), _dev_ptr(k), _dev_ptr(v), _dev_ptr(o), B, H, L, d,
                                    float(scale), int(causal), dtype_code(q), _dev_ptr(workspace),

@@ -121,9 +121,21 @@ struct StreamWorkspace {
   size_t bytes = 0;
 };
 
+// A forward plan: the derived tiles of one shape and the compiled instance
+// that runs them.  The derivation is a pure function of the device's
+// descriptor and the shape, so each device keeps the plans of the shapes it
+// has run (at most kMaxPlans, then the table starts over).
+struct FwdPlan {
+  attn_tile_report_t rep;
+  const FwdInstance* inst;
+};
+using PlanKey = std::tuple<int, int, int, int, int, int>;  // B, H, L, d, causal, dtype
+constexpr size_t kMaxPlans = 1024;
+
 struct DeviceState {
   bool have_desc = false;
   attn_hw_desc_t desc{};
+  std::map<PlanKey, FwdPlan> plans;
   std::map<hipStream_t, StreamWorkspace> ws;
   std::vector<void*> retired;
 };
@@ -221,6 +233,31 @@ int plan(const attn_hw_desc_t* hw, int B, int H, int L, int d, int causal, int d
   return ATTN_OK;
 }
 
+// The plan of a shape on the given device: derived on the device's first
+// call with that shape, then read from its table.
+int device_plan(int device, int B, int H, int L, int d, int causal, int dtype, attn_tile_report_t* rep,
+                const FwdInstance** inst) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  DeviceState& st = g_dev[device];
+  if (!st.have_desc) {
+    const int rc = query_desc(device, &st.desc);
+    if (rc != ATTN_OK) return rc;
+    st.have_desc = true;
+  }
+  const PlanKey key{B, H, L, d, causal != 0, dtype};
+  const auto it = st.plans.find(key);
+  if (it != st.plans.end()) {
+    *rep = it->second.rep;
+    *inst = it->second.inst;
+    return ATTN_OK;
+  }
+  const int rc = plan(&st.desc, B, H, L, d, causal, dtype, rep, inst);
+  if (rc != ATTN_OK) return rc;
+  if (st.plans.size() >= kMaxPlans) st.plans.clear();
+  st.plans.emplace(key, FwdPlan{*rep, *inst});
+  return ATTN_OK;
+}
+
 }  // namespace
 
 namespace attn {
@@ -235,10 +272,7 @@ int prepare(const void* Q, const void* K, const void* V, void* O, int B, int H, 
   if (rc != ATTN_OK) return rc;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return ATTN_E_HIP;
-  attn_hw_desc_t desc;
-  rc = device_desc(dev, &desc);
-  if (rc != ATTN_OK) return rc;
-  rc = plan(&desc, B, H, L, d, causal, dtype, &out->rep, &out->inst);
+  rc = device_plan(dev, B, H, L, d, causal, dtype, &out->rep, &out->inst);
   if (rc != ATTN_OK) return rc;
   FwdParams& p = out->p;
   p = FwdParams{};
