@@ -302,6 +302,7 @@ def main():
     ap.add_argument("--no-d96", action="store_true", help="skip the head-dimension-96 workloads")
     ap.add_argument("--no-d64", action="store_true", help="skip the head-dimension-64 workloads")
     ap.add_argument("--no-causal-few", action="store_true", help="skip the few-head causal workloads")
+    ap.add_argument("--no-short", action="store_true", help="skip the many-head short-sequence workloads")
     ap.add_argument("--no-softmax", action="store_true", help="skip the row-softmax operator")
     ap.add_argument("--no-gemm", action="store_true", help="skip the GEMM operator")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -401,7 +402,8 @@ def main():
                               "frac_at_counter_clock": at_clock(ach, mc2), "mfma_counters": mc2},
                  "algorithmic_flops": fl2, "algorithmic_bytes": fused_bytes(w2),
                  "tiles": {"t_kv": p2.t_kv, "t_q_wave": p2.t_q_wave, "n_waves": p2.n_waves,
-                           "n_split": p2.n_split, "grid": p2.grid, "binding": p2.binding.decode()}}
+                           "n_split": p2.n_split, "grid": p2.grid, "launch_grid": p2.launch_grid,
+                           "binding": p2.binding.decode()}}
         del ws2
         if with_unfused:
             wsu = torch.empty(capi.attn_unfused_workspace_bytes(w2.B, w2.H, w2.L, dt2), dtype=torch.uint8,
@@ -476,7 +478,7 @@ def main():
                         "pct_peak": round(100 * flops(w3) / (ev3 * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 1),
                         "tiles": {"t_kv": p3.t_kv, "t_q_wave": p3.t_q_wave, "n_waves": p3.n_waves,
                                   "n_split": p3.n_split, "tiles_per_split": p3.tiles_per_split,
-                                  "grid": p3.grid}})
+                                  "grid": p3.grid, "launch_grid": p3.launch_grid}})
             del t3, o3
             torch.cuda.empty_cache()
         return out
@@ -485,6 +487,7 @@ def main():
     d96 = None if args.no_d96 else head_dim_leg(inputs.HEAD_DIM_96)
     d64 = None if args.no_d64 else head_dim_leg(inputs.HEAD_DIM_64)
     causal_few = None if args.no_causal_few else head_dim_leg(inputs.CAUSAL_FEW_HEADS)
+    short = None if args.no_short else head_dim_leg(inputs.SHORT_SEQUENCES)
 
     smx = None
     if not args.no_softmax:
@@ -618,6 +621,7 @@ def main():
         "head_dim_96": d96,
         "head_dim_64": d64,
         "causal_few_heads": causal_few,
+        "short_sequences": short,
         "softmax": smx,
         "gemm": gemm,
         "cpu_baseline": cpu,

@@ -126,6 +126,12 @@ typedef struct {
   int32_t low_occupancy;        /* grid < num_cus */
   int32_t lds_bw_ok;            /* t_q_wave * lds_bytes_per_clk >= mfma_flops_per_clk_cu */
   char binding[16];             /* "LDS", "VGPR", "CU" or "atom" */
+  int64_t launch_grid;          /* workgroups the fused kernel is launched with: grid, or (from
+                                   attn_fwd_plan) one per CU when attn_fwd runs the query tiles
+                                   as a persistent launch, each workgroup taking a fixed list of
+                                   them back to back (no split, more query tiles than CUs, each
+                                   at least 4 and on average at most 24 key tiles long; d = 64
+                                   and 128).  The derivation itself sets it to grid. */
 } attn_tile_report_t;
 
 /* Fill `out` with a named descriptor: "paper_gpu_a" and "paper_gpu_b" (the two
@@ -174,7 +180,10 @@ int attn_fwd_plan(const attn_hw_desc_t* hw, int B, int H, int L, int d, int caus
  * standard attention).  causal != 0 keeps keys j <= i for query i (top-left
  * aligned).  When the derivation splits the key range (split-N, Section 5.3),
  * a second kernel merges the splits' partial results with the Section 5.3
- * operator.
+ * operator.  Plans whose report has launch_grid < grid run persistent: one
+ * workgroup per CU, each taking its share of the query tiles back to back
+ * (the result is the same, bit for bit).  The plan of each shape is derived
+ * once per device and kept (at most 1024 shapes, then the table starts over).
  * Ownership and ordering: the call only enqueues work on `stream`; it never
  * synchronises.  The merge's workspace belongs to the library: one buffer per
  * (device, stream), so concurrent calls on different streams never share

@@ -80,7 +80,8 @@ class TileReport(_Struct):
                 ("n_waves", c_int32), ("tile_q", c_int32), ("n_split", c_int32),
                 ("tiles_per_split", c_int32), ("grid", c_int64), ("vgpr_est", c_int32), ("vgpr_budget", c_int32),
                 ("lds_used", c_int64), ("lds_budget", c_int64), ("wg_per_cu", c_double),
-                ("low_occupancy", c_int32), ("lds_bw_ok", c_int32), ("binding", c_char * 16)]
+                ("low_occupancy", c_int32), ("lds_bw_ok", c_int32), ("binding", c_char * 16),
+                ("launch_grid", c_int64)]
 
 
 class SoftmaxReport(_Struct):

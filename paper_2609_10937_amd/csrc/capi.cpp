@@ -3,6 +3,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <algorithm>
 #include <map>
 #include <mutex>
 #include <tuple>
@@ -218,6 +219,35 @@ int make_op(int B, int H, int L, int d, int causal, int dtype, attn_op_t* op) {
   return ATTN_OK;
 }
 
+// Persistent launches (the fused kernel's PERSIST variant: one workgroup per
+// CU running a fixed list of query tiles back to back) for plans without
+// split key ranges that have more query tiles than CUs (num_cus a multiple
+// of 8, the XCD count), every query tile at least kPersistMinTiles key tiles
+// long (the unit switch keeps the copies in flight within the current and
+// the next tile), at most kPersistMaxMeanTiles on average, and the byte
+// offsets of a head's rows, up to the end of its last query tile, below
+// 4 GiB (its buffer descriptors).  The mean bound is measured: a query tile
+// of a workgroup's own costs about as much as 6 to 9 key tiles, which the
+// persistent schedule hides, while its loop runs a few percent slower per
+// key tile; at 16 key tiles per query tile (L = 1024, d = 128) it gains 8%,
+// at 32 nothing, and at the configurations with 34 and 130 it loses 3 to 7%.
+constexpr int kPersistMinTiles = 4, kPersistMaxMeanTiles = 24;
+
+bool persistent(const attn_tile_report_t& rep, const FwdInstance* inst, int L, int d, int causal, int num_cus) {
+  if (!inst->launch_persist || rep.n_split != 1 || num_cus <= 0 || num_cus % 8 != 0) return false;
+  if (rep.grid <= num_cus) return false;
+  if ((int64_t)(L + rep.tile_q) * d * 2 >= ((int64_t)1 << 32)) return false;
+  const int64_t n_kv = (L + rep.t_kv - 1) / rep.t_kv, n_qt = (L + rep.tile_q - 1) / rep.tile_q;
+  int64_t shortest = n_kv, total = n_kv * n_qt;
+  if (causal) {
+    total = 0;
+    for (int64_t qt = 0; qt < n_qt; ++qt)
+      total += std::min(n_kv, (std::min<int64_t>(L, (qt + 1) * rep.tile_q) + rep.t_kv - 1) / rep.t_kv);
+    shortest = std::min(n_kv, (std::min<int64_t>(L, rep.tile_q) + rep.t_kv - 1) / rep.t_kv);
+  }
+  return shortest >= kPersistMinTiles && total <= (int64_t)kPersistMaxMeanTiles * n_qt;
+}
+
 int plan(const attn_hw_desc_t* hw, int B, int H, int L, int d, int causal, int dtype, attn_tile_report_t* rep,
          const FwdInstance** inst) {
   attn_op_t op;
@@ -230,6 +260,7 @@ int plan(const attn_hw_desc_t* hw, int B, int H, int L, int d, int causal, int d
   if (!f) return ATTN_E_NO_INSTANCE;
   if (inst) *inst = f;
   if (rep->grid > 0x7fffffffLL) return ATTN_E_SHAPE;
+  if (persistent(*rep, f, L, d, causal, hw->num_cus)) rep->launch_grid = hw->num_cus;
   return ATTN_OK;
 }
 
@@ -296,6 +327,11 @@ int prepare(const void* Q, const void* K, const void* V, void* O, int B, int H, 
   const size_t rows = (size_t)p.n_split * p.BH * L;
   out->ws_bytes = p.n_split > 1 ? rows * (size_t)d * 2 + rows * 8 : 0;
   return ATTN_OK;
+}
+
+hipError_t launch_fused(const Prepared& pr, hipStream_t s) {
+  const bool persist = pr.rep.launch_grid != pr.rep.grid;
+  return (persist ? pr.inst->launch_persist : pr.inst->launch)(pr.p, (unsigned)pr.rep.launch_grid, s);
 }
 
 void bind_workspace(FwdParams& p, void* ws, int d) {
@@ -432,7 +468,7 @@ int attn_fwd(const void* Q, const void* K, const void* V, void* O, int B, int H,
   int rc = prepare(Q, K, V, O, B, H, L, d, scale, causal, dtype, &pr);
   if (rc != ATTN_OK) return rc;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (pr.ws_bytes == 0) return pr.inst->launch(pr.p, (unsigned)pr.rep.grid, s) == hipSuccess ? ATTN_OK : ATTN_E_HIP;
+  if (pr.ws_bytes == 0) return launch_fused(pr, s) == hipSuccess ? ATTN_OK : ATTN_E_HIP;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return ATTN_E_HIP;
   // The lock covers binding the stream's buffer and enqueueing both kernels,
@@ -453,7 +489,7 @@ int attn_fwd(const void* Q, const void* K, const void* V, void* O, int B, int H,
     w.bytes = grow;
   }
   bind_workspace(pr.p, w.ptr, d);
-  if (pr.inst->launch(pr.p, (unsigned)pr.rep.grid, s) != hipSuccess) return ATTN_E_HIP;
+  if (launch_fused(pr, s) != hipSuccess) return ATTN_E_HIP;
   return launch_combine(pr.p, d, dtype, s) == hipSuccess ? ATTN_OK : ATTN_E_HIP;
 }
 
@@ -478,7 +514,7 @@ int attn_fwd_partial(const void* Q, const void* K, const void* V, void* O, int B
     if (!aligned16(workspace)) return ATTN_E_ALIGN;
     bind_workspace(pr.p, workspace, d);
   }
-  return pr.inst->launch(pr.p, (unsigned)pr.rep.grid, static_cast<hipStream_t>(stream)) == hipSuccess ? ATTN_OK
+  return launch_fused(pr, static_cast<hipStream_t>(stream)) == hipSuccess ? ATTN_OK
                                                                                                    : ATTN_E_HIP;
 }
 

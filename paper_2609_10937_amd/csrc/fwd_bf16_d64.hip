@@ -1,13 +1,15 @@
 // Fused-kernel instantiations for dtype bf16, head dimension 64 (t_kv = 128,
 // 5 LDS stages): every (query blocks per wave, waves per workgroup) the tile
-// derivation can reach for this head dimension on a gfx950 descriptor.
+// derivation can reach for this head dimension on a gfx950 descriptor, and
+// the 8-wave one also as a persistent launch.
 #include "fwd_kernel.hpp"
 
 namespace attn {
 
 const FwdInstance* fwd_instances_bf16_d64(int* n) {
   static const FwdInstance table[] = {
-      {ATTN_BF16, 64, 128, 2, 8, launch_fwd<ATTN_BF16, 64, 128, 2, 8, 5>},
+      {ATTN_BF16, 64, 128, 2, 8, launch_fwd<ATTN_BF16, 64, 128, 2, 8, 5>,
+       launch_fwd<ATTN_BF16, 64, 128, 2, 8, 5, true>},
       {ATTN_BF16, 64, 128, 2, 4, launch_fwd<ATTN_BF16, 64, 128, 2, 4, 5>},
       {ATTN_BF16, 64, 128, 2, 2, launch_fwd<ATTN_BF16, 64, 128, 2, 2, 5>},
       {ATTN_BF16, 64, 128, 2, 1, launch_fwd<ATTN_BF16, 64, 128, 2, 1, 5>},

@@ -44,6 +44,12 @@
 // step ends with a workgroup barrier; the operand reads of a matrix phase
 // are software-pipelined PF fragments ahead of the products that use them.
 //
+// PERSIST = true is the same kernel as a persistent launch, one workgroup per
+// CU, for launches of many short query tiles: each workgroup runs a fixed list
+// of query tiles back to back through one ring of K/V tiles, so the next
+// tile's first key tiles and Q rows load while the current one finishes
+// instead of after its workgroup has left the CU.
+//
 // Softmax bookkeeping keeps a per-row reference max m that is only raised
 // when a score would give a weight above 2^8 (the merge of Section 5.3 holds
 // for any common reference point, so the result is the same).  Most tiles
@@ -312,7 +318,7 @@ __device__ __forceinline__ void softmax_tile(f32x4_t (&s)[NKB][QB], typename M::
     for (int pp = 0; pp < NP; ++pp) asm volatile("" : "+v"(pk[pp][qb]));
 }
 
-template <int DT, int D, int TKV, int QB, int NW, int ST>
+template <int DT, int D, int TKV, int QB, int NW, int ST, bool PERSIST>
 __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   using M = Mfma<DT>;
   using V8 = typename M::V8;
@@ -418,43 +424,61 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
       placed = true;
     }
   }
-  if (!placed) {
+  // Workgroup b of the order above -> (head, split, query tile).
+  auto decode = [&](int b, int& hd_out, int& sp_out, int& qt_out) ATTN_INLINE {
     int unit, rank;
     if (order == kOrderUnits) {
-      const int x = blockIdx.x % 8, i = blockIdx.x / 8;
+      const int x = b % 8, i = b / 8;
       const int per_group = xg * p.n_qt;
       const int gi = i / per_group, r = i - gi * per_group;
       rank = r / xg;
       unit = x + 8 * (gi * xg + (r - rank * xg));
     } else if (order == kOrderTiles) {
-      const int x = blockIdx.x % 8, i = blockIdx.x / 8;
+      const int x = b % 8, i = b / 8;
       const int sp = i % p.n_split;
       const int t = (i / p.n_split) * 8 + x;
       const int hd = t / p.n_qt;
       rank = t - hd * p.n_qt;
       unit = hd * p.n_split + sp;
     } else {
-      rank = blockIdx.x / units;
-      unit = blockIdx.x - rank * units;
+      rank = b / units;
+      unit = b - rank * units;
     }
-    head = unit / p.n_split;
-    split = unit - head * p.n_split;
-    qt = p.causal ? (p.n_qt - 1 - rank) : rank;
+    hd_out = unit / p.n_split;
+    sp_out = unit - hd_out * p.n_split;
+    qt_out = p.causal ? (p.n_qt - 1 - rank) : rank;
+  };
+
+  // Persistent launch (PERSIST: one workgroup per CU, without split key
+  // ranges).  The workgroups b = 8 i + x that the order above puts on XCD x
+  // become units of work shared by the launch's S = gridDim.x / 8 workgroups
+  // on that XCD, in rounds taken snake-wise: in round r slot s takes item
+  // r S + s when r is even and r S + S - 1 - s when r is odd, so that a
+  // heavy causal query tile of one round pairs with a light one of the next.
+  // A workgroup runs its units back to back through one ring of K/V tiles.
+  [[maybe_unused]] const int px = blockIdx.x % 8, ps = blockIdx.x / 8, pS = gridDim.x / 8;
+  [[maybe_unused]] const int p_items = PERSIST ? (p.BH * p.n_qt - px + 7) / 8 : 0;
+  [[maybe_unused]] auto p_item = [&](int r) ATTN_INLINE { return r * pS + ((r & 1) ? pS - 1 - ps : ps); };
+  if constexpr (PERSIST) {
+    if (p_item(0) >= p_items) return;  // no unit here (the whole workgroup leaves before any barrier)
+    decode(8 * p_item(0) + px, head, split, qt);
+  } else if (!placed) {
+    decode(blockIdx.x, head, split, qt);
   }
 
-  const size_t hoff = (size_t)head * (size_t)L * D;
+  size_t hoff = (size_t)head * (size_t)L * D;
   const uint16_t* __restrict__ Qh = static_cast<const uint16_t*>(p.q) + hoff;
   const uint16_t* __restrict__ Kh = static_cast<const uint16_t*>(p.k) + hoff;
   const uint16_t* __restrict__ Vh = static_cast<const uint16_t*>(p.v) + hoff;
 
-  const int q_wg = qt * TILE_Q;
-  const int q0 = q_wg + w * TQW;
-
-  int n_kv = (L + TKV - 1) / TKV;
-  if (p.causal) {
-    const int last = min(L, q_wg + TILE_Q);
-    n_kv = min(n_kv, (last + TKV - 1) / TKV);
-  }
+  // Key tiles query tile qt_ sees (causal: up to its last row).
+  auto tiles_of = [&](int qt_) ATTN_INLINE {
+    int nk = (L + TKV - 1) / TKV;
+    if (p.causal) nk = min(nk, (min(L, qt_ * TILE_Q + TILE_Q) + TKV - 1) / TKV);
+    return nk;
+  };
+  int q0 = qt * TILE_Q + w * TQW;
+  const int n_kv = tiles_of(qt);
   const int t_begin = split * p.tiles_per_split;
   const int n = min(n_kv, t_begin + p.tiles_per_split) - t_begin;  // tiles of this workgroup
 
@@ -501,9 +525,15 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
     koff[i] = block_off(i, false);
     voff[i] = block_off(i, true);
   }
-  const uint64_t kh_base = uniform_ptr(Kh), vh_base = uniform_ptr(Vh);
+  uint64_t kh_base = uniform_ptr(Kh), vh_base = uniform_ptr(Vh);
   // Key rows this workgroup reads: its split's range, clipped to the sequence.
-  const int kv_end = __builtin_amdgcn_readfirstlane(min(L, (t_begin + max(n, 0)) * TKV));
+  int kv_end = __builtin_amdgcn_readfirstlane(min(L, (t_begin + max(n, 0)) * TKV));
+  // PERSIST: tile indices j count over all of the workgroup's units; the
+  // current unit holds j in [cur_start, cur_end), the next one (if any)
+  // starts at nx_start = cur_end and has its own bases and key range
+  // (nx_kv_end = 0 when there is none, so tiles past the last unit are empty).
+  [[maybe_unused]] int cur_start = 0, cur_end = n, nx_start = n, nx_kv_end = 0;
+  [[maybe_unused]] uint64_t nkh = kh_base, nvh = vh_base;
   // This wave's part of tile j: its LPW blocks of the K image and of the V
   // image, as copies 0 .. NC-1 (copy 2i is block i of K, 2i+1 block i of V);
   // issue(j, lo, hi) makes copies lo .. hi-1.
@@ -513,10 +543,19 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
     i32x4_t k, v;
   };
   auto tile_rsrc = [&](int j) ATTN_INLINE -> TileRsrc {
-    const int kv0 = (t_begin + j) * TKV;
-    const uint32_t bytes = (uint32_t)max(0, min(kv_end - kv0, TKV)) * GROWB;
-    return TileRsrc{buffer_rsrc(kh_base + (uint64_t)kv0 * GROWB, bytes),
-                    buffer_rsrc(vh_base + (uint64_t)kv0 * GROWB, bytes)};
+    uint64_t kb = kh_base, vb = vh_base;
+    int kv0 = (t_begin + j) * TKV, end = kv_end;
+    if constexpr (PERSIST) {
+      kv0 = (j - cur_start) * TKV;
+      if (j >= cur_end) {
+        kb = nkh;
+        vb = nvh;
+        kv0 = (j - nx_start) * TKV;
+        end = nx_kv_end;
+      }
+    }
+    const uint32_t bytes = (uint32_t)max(0, min(end - kv0, TKV)) * GROWB;
+    return TileRsrc{buffer_rsrc(kb + (uint64_t)kv0 * GROWB, bytes), buffer_rsrc(vb + (uint64_t)kv0 * GROWB, bytes)};
   };
   auto issue_r = [&](const TileRsrc& rs, int j, int lo, int hi) ATTN_INLINE {
     const i32x4_t kr = rs.k, vr = rs.v;
@@ -627,7 +666,7 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   // queue at once.  Tiles past the range are copied too (in-bounds rows, into
   // stages no later phase reads), which keeps the phase one basic block and
   // the copy count per step constant.
-  auto mphase = [&](auto g2c, auto g1c, int j, int jc) ATTN_INLINE {
+  auto mphase = [&](auto g2c, auto g1c, int j, int jc, const V8 (&qa)[QB][KC]) ATTN_INLINE {
     constexpr bool G2 = decltype(g2c)::value, G1 = decltype(g1c)::value;
     constexpr int F = (G2 ? NVF : 0) + (G1 ? NKF : 0);
     const uint32_t Vs = vbase + (uint32_t)__builtin_amdgcn_readfirstlane(lds0 + ((j + ST - 1) % ST) * STAGEB + TILEB);
@@ -672,7 +711,7 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
         const int kc = fk / NKB, kb = fk % NKB;
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb)
-          s[kb][qb] = M::run(buf[f], qf[qb][kc], kc == 0 ? (f32x4_t){0.f, 0.f, 0.f, 0.f} : s[kb][qb]);
+          s[kb][qb] = M::run(buf[f], qa[qb][kc], kc == 0 ? (f32x4_t){0.f, 0.f, 0.f, 0.f} : s[kb][qb]);
       }
       if (f + PF < F) buf[f + PF] = load(f + PF);
       if constexpr (G1) {
@@ -701,11 +740,50 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   // Vector phase S(j): the softmax of tile j.  Only tiles that cross the
   // causal diagonal or the end of the sequence take the masked body.
   auto sphase = [&](int j) ATTN_INLINE {
-    const int kv0 = (t_begin + j) * TKV;
+    int kv0 = (t_begin + j) * TKV;
+    if constexpr (PERSIST) kv0 = (j - cur_start) * TKV;
     if ((kv0 + TKV > L) || (p.causal && kv0 + TKV - 1 > q0))
       softmax_tile<true, M>(s, pk, mref, lim, corr, rescale, kv0, q0, g, c, L, p.causal, cs);
     else
       softmax_tile<false, M>(s, pk, mref, lim, corr, rescale, kv0, q0, g, c, L, p.causal, cs);
+  };
+
+  // Epilogue.  Each of the four lane groups holds a partial row sum over its
+  // key subset (same reference), so the total is their sum.  Without a split
+  // O / sum is rounded to the input type and stored.  A split stores the same
+  // normalised output of its key range (a convex combination of V rows, so in
+  // the range of the input type), and beside it, in fp32, its reference (base
+  // 2, -inf for a row that saw no key) and its sum, which the merge needs to
+  // weigh the splits.
+  auto pack4 = [&](const f32x4_t& v) ATTN_INLINE -> u32x2_t {
+    S h4[4] = {(S)v[0], (S)v[1], (S)v[2], (S)v[3]};
+    const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, h4[0]) |
+                        ((uint32_t)__builtin_bit_cast(uint16_t, h4[1]) << 16);
+    const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, h4[2]) |
+                        ((uint32_t)__builtin_bit_cast(uint16_t, h4[3]) << 16);
+    return (u32x2_t){lo, hi};
+  };
+  auto store_row = [&](uint16_t* row, const f32x4_t (&acc)[NDB], float inv) ATTN_INLINE {
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) *reinterpret_cast<u32x2_t*>(row + 16 * db + 4 * g) = pack4(acc[db] * inv);
+  };
+  // PERSIST: the current unit's rows (no split), through a buffer descriptor
+  // over its head's O, so rows past the sequence are dropped by the
+  // descriptor's range and every wave issues exactly QB * NDB stores (the
+  // waits of the unit switch count them).
+  [[maybe_unused]] auto store_unit_rows = [&]() ATTN_INLINE {
+    const __amdgpu_buffer_rsrc_t ors = __builtin_amdgcn_make_buffer_rsrc(
+        reinterpret_cast<void*>(uniform_ptr(static_cast<uint16_t*>(p.o) + hoff)), (short)0,
+        __builtin_amdgcn_readfirstlane((int)((uint32_t)L * (uint32_t)(D * 2))), 0x00020000);
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      const float lt = lacc[qb][0];
+      const float inv = lt > 0.f ? 1.f / lt : 0.f;
+      const uint32_t rowb = (uint32_t)(q0 + 16 * qb + c) * (uint32_t)(D * 2) + 8u * (uint32_t)g;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+        __builtin_amdgcn_raw_buffer_store_b64(pack4(o[qb][db] * inv), ors, (int)(rowb + 32u * (uint32_t)db), 0, 0);
+    }
   };
 
   // Phase schedule.  M(j) is the matrix phase of tile j (GEMM2 of tile j-1
@@ -722,79 +800,186 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   // has its part of tile j + 1 complete before B(j + 1); the barrier then
   // publishes the whole tile to M(j + 1) of both groups.
   if (n > 0) {
-    auto matrix = [&](auto g2c, auto g1c, int j) ATTN_INLINE {
+    auto matrix = [&](auto g2c, auto g1c, int j, const V8 (&qa)[QB][KC]) ATTN_INLINE {
       __builtin_amdgcn_s_setprio(1);
-      mphase(g2c, g1c, j, j + 1 + AHEAD);
+      mphase(g2c, g1c, j, j + 1 + AHEAD, qa);
       __builtin_amdgcn_s_setprio(0);
     };
     const std::false_type no{};
     const std::true_type yes{};
     lds_barrier();  // B(0)
-    // End of a wave's step j: its part of tile j + 1 complete, then the
-    // barrier.  Group 1's steps end after its matrix phases, group 0's after
-    // its vector phases; the phases themselves are one straight sequence.
-    auto end_step = [&](int j, int last_issued) ATTN_INLINE {
-      if (j + 1 < n) wait_tile(j + 1, last_issued);
-      lds_barrier();
-    };
-    matrix(no, yes, 0);
-    if (grp == 1) end_step(0, 1 + AHEAD);
-    sphase(0);
-    if (grp == 0) end_step(0, 1 + AHEAD);
-    for (int j = 1; j < n; ++j) {
-      matrix(yes, yes, j);
-      if (grp == 1) end_step(j, j + 1 + AHEAD);
-      sphase(j);
-      if (grp == 0) end_step(j, j + 1 + AHEAD);
+    if constexpr (!PERSIST) {
+      // End of a wave's step j: its part of tile j + 1 complete, then the
+      // barrier.  Group 1's steps end after its matrix phases, group 0's after
+      // its vector phases; the phases themselves are one straight sequence.
+      auto end_step = [&](int j, int last_issued) ATTN_INLINE {
+        if (j + 1 < n) wait_tile(j + 1, last_issued);
+        lds_barrier();
+      };
+      matrix(no, yes, 0, qf);
+      if (grp == 1) end_step(0, 1 + AHEAD);
+      sphase(0);
+      if (grp == 0) end_step(0, 1 + AHEAD);
+      for (int j = 1; j < n; ++j) {
+        matrix(yes, yes, j, qf);
+        if (grp == 1) end_step(j, j + 1 + AHEAD);
+        sphase(j);
+        if (grp == 0) end_step(j, j + 1 + AHEAD);
+      }
+      matrix(yes, no, n, qf);
+    } else {
+      // Units back to back.  The tiles of the next unit are requested like
+      // any tile, AHEAD + 1 matrix phases before their own; its Q rows at
+      // the start of M(J - 2), J = nx_start its first tile, into qn.  M(J)
+      // runs the second product of the finished unit's last tile beside the
+      // first product of the new unit (on qn, which becomes qf), and right
+      // after it each wave stores the finished unit's rows and starts the
+      // statistics over: group 1's S(J - 1) still belongs to the old unit,
+      // group 0's S(J) to the new one.  Every unit has at least AHEAD + 2
+      // tiles (the host checks), so the copies and the Q rows in flight
+      // belong to the current or the next unit only.
+      static_assert(AHEAD == 2, "the switch's waits assume two tiles requested ahead");
+      constexpr int NST = QB * NDB;  // store instructions of a unit's rows, per wave
+      constexpr int QL = QB * KC;    // load instructions of a unit's Q rows, per wave
+      static_assert(4 * LPW + NST + QL < 64, "vmcnt range");
+      int r = 0;  // round of the current unit
+      bool nx_valid = false;
+      int nx_head = 0, nx_qt = 0, nx_n = 0;
+      auto set_next = [&]() ATTN_INLINE {
+        nx_start = cur_end;
+        const int it = p_item(r + 1);
+        nx_valid = it < p_items;
+        nx_kv_end = 0;
+        nkh = kh_base;
+        nvh = vh_base;
+        if (nx_valid) {
+          int sp;
+          decode(8 * it + px, nx_head, sp, nx_qt);
+          nx_n = tiles_of(nx_qt);
+          const size_t ho = (size_t)nx_head * (size_t)L * D;
+          nkh = uniform_ptr(static_cast<const uint16_t*>(p.k) + ho);
+          nvh = uniform_ptr(static_cast<const uint16_t*>(p.v) + ho);
+          nx_kv_end = __builtin_amdgcn_readfirstlane(min(L, nx_n * TKV));
+        }
+      };
+      set_next();
+      V8 qn[QB][KC];
+      // The next unit's Q fragments: one 16-byte buffer load each (rows past
+      // the sequence read as zeros).
+      auto load_next_q = [&]() ATTN_INLINE {
+        const __amdgpu_buffer_rsrc_t qrs = __builtin_amdgcn_make_buffer_rsrc(
+            reinterpret_cast<void*>(uniform_ptr(static_cast<const uint16_t*>(p.q) + (size_t)nx_head * (size_t)L * D)),
+            (short)0, __builtin_amdgcn_readfirstlane((int)((uint32_t)L * (uint32_t)(D * 2))), 0x00020000);
+        const uint32_t rowb = (uint32_t)(nx_qt * TILE_Q + w * TQW + c) * (uint32_t)(D * 2) + 16u * (uint32_t)g;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+          for (int kc = 0; kc < KC; ++kc)
+            qn[qb][kc] = __builtin_bit_cast(
+                V8, __builtin_amdgcn_raw_buffer_load_b128(
+                        qrs, (int)(rowb + (uint32_t)(16 * qb) * (uint32_t)(D * 2) + 64u * (uint32_t)kc), 0, 0));
+        __builtin_amdgcn_sched_barrier(0);
+      };
+      int last_switch = -8;  // step of the last switch (the finished unit's rows stored after its M)
+      // End of step j: this wave's part of tile j + 1 complete, then the
+      // barrier.  The copies of tile j + 1 were requested in M(j - 2); the
+      // wait counts the operations issued after them (they complete in issue
+      // order): two tiles of copies, plus the next unit's Q loads (issued at
+      // the start of M(s - 2) for a switch at step s: steps s - 2 and s - 1)
+      // and the last unit's stores (after M(s): steps s to s + 2).  The last
+      // step waits for a tile past the range, whose copies are empty.
+      auto end_step_p = [&](int j) ATTN_INLINE {
+        const int e = j - (nx_valid && nx_start - j <= 2 ? nx_start : last_switch);
+        if (e >= -2 && e <= 2) {
+          if (e < 0) wait_vmcnt<4 * LPW + QL>();
+          else wait_vmcnt<4 * LPW + NST>();
+        } else {
+          wait_vmcnt<4 * LPW>();
+        }
+        lds_barrier();
+      };
+      matrix(no, yes, 0, qf);
+      if (grp == 1) end_step_p(0);
+      sphase(0);
+      if (grp == 0) end_step_p(0);
+      for (int j = 1;; ++j) {
+        const bool sw_now = j == nx_start;
+        if (sw_now && !nx_valid) break;  // the last unit's tiles are done
+        if (nx_valid && j + 2 == nx_start) load_next_q();
+        if (sw_now) {
+          // The compiler waits for the Q loads here (and with them for every
+          // copy requested before this point: they complete in issue order).
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+            for (int kc = 0; kc < KC; ++kc) qf[qb][kc] = qn[qb][kc];
+        }
+        matrix(yes, yes, j, qf);
+        if (sw_now) {
+          store_unit_rows();
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb) {
+            mref[qb] = 0.f;
+            lim[qb] = -INFINITY;
+            corr[qb] = 1.f;
+            lacc[qb] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int db = 0; db < NDB; ++db) o[qb][db] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+          }
+          rescale = false;
+          head = nx_head;
+          qt = nx_qt;
+          hoff = (size_t)head * (size_t)L * D;
+          q0 = qt * TILE_Q + w * TQW;
+          kh_base = nkh;
+          vh_base = nvh;
+          kv_end = nx_kv_end;
+          cur_start = j;
+          cur_end = j + nx_n;
+          ++r;
+          set_next();
+          last_switch = j;
+        }
+        if (grp == 1) end_step_p(j);
+        sphase(j);
+        if (grp == 0) end_step_p(j);
+      }
+      matrix(yes, no, cur_end, qf);
     }
-    matrix(yes, no, n);
     // The copies of the tiles past the range land before the workgroup's
     // LDS is released.
     wait_vmcnt<0>();
   }
 
-  // Epilogue.  Each of the four lane groups holds a partial row sum over its
-  // key subset (same reference), so the total is their sum.  Without a split
-  // O / sum is rounded to the input type and stored.  A split stores the same
-  // normalised output of its key range (a convex combination of V rows, so in
-  // the range of the input type), and beside it, in fp32, its reference (base
-  // 2, -inf for a row that saw no key) and its sum, which the merge needs to
-  // weigh the splits.
-  auto store_row = [&](uint16_t* row, const f32x4_t (&acc)[NDB], float inv) ATTN_INLINE {
+  if constexpr (PERSIST) {
+    store_unit_rows();
+  } else {
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-      const f32x4_t v = acc[db] * inv;
-      S h4[4] = {(S)v[0], (S)v[1], (S)v[2], (S)v[3]};
-      const uint32_t lo = (uint32_t)__builtin_bit_cast(uint16_t, h4[0]) |
-                          ((uint32_t)__builtin_bit_cast(uint16_t, h4[1]) << 16);
-      const uint32_t hi = (uint32_t)__builtin_bit_cast(uint16_t, h4[2]) |
-                          ((uint32_t)__builtin_bit_cast(uint16_t, h4[3]) << 16);
-      *reinterpret_cast<u32x2_t*>(row + 16 * db + 4 * g) = (u32x2_t){lo, hi};
-    }
-  };
-#pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    const float lt = lacc[qb][0];
-    const float inv = lt > 0.f ? 1.f / lt : 0.f;
-    int q = q0 + 16 * qb + c;
-    // Row offsets at a d that is not a power of two are multiplications: keep
-    // the compiler from carrying the Q loads' ones through the loop.
-    if constexpr (D != DL) asm volatile("" : "+v"(q));
-    if (q >= L) continue;
-    if (p.n_split == 1) {
-      store_row(static_cast<uint16_t*>(p.o) + hoff + (size_t)q * D, o[qb], inv);
-    } else {
-      const size_t prow = ((size_t)split * p.BH + head) * (size_t)L + q;
-      store_row(static_cast<uint16_t*>(p.part_o) + prow * D, o[qb], inv);
-      if (g == 0)
-        *reinterpret_cast<float2*>(p.part_ml + prow * 2) = make_float2(lim[qb] == -INFINITY ? -INFINITY : mref[qb], lt);
+    for (int qb = 0; qb < QB; ++qb) {
+      const float lt = lacc[qb][0];
+      const float inv = lt > 0.f ? 1.f / lt : 0.f;
+      int q = q0 + 16 * qb + c;
+      // Row offsets at a d that is not a power of two are multiplications: keep
+      // the compiler from carrying the Q loads' ones through the loop.
+      if constexpr (D != DL) asm volatile("" : "+v"(q));
+      if (q >= L) continue;
+      if (p.n_split == 1) {
+        store_row(static_cast<uint16_t*>(p.o) + hoff + (size_t)q * D, o[qb], inv);
+      } else {
+        const size_t prow = ((size_t)split * p.BH + head) * (size_t)L + q;
+        store_row(static_cast<uint16_t*>(p.part_o) + prow * D, o[qb], inv);
+        if (g == 0)
+          *reinterpret_cast<float2*>(p.part_ml + prow * 2) =
+              make_float2(lim[qb] == -INFINITY ? -INFINITY : mref[qb], lt);
+      }
     }
   }
 }
 
-template <int DT, int D, int TKV, int QB, int NW, int ST>
+template <int DT, int D, int TKV, int QB, int NW, int ST, bool PERSIST = false>
 hipError_t launch_fwd(const FwdParams& p, unsigned grid, hipStream_t s) {
-  hipLaunchKernelGGL((fwd_kernel<DT, D, TKV, QB, NW, ST>), dim3(grid), dim3(NW * 64), 0, s, p);
+  hipLaunchKernelGGL((fwd_kernel<DT, D, TKV, QB, NW, ST, PERSIST>), dim3(grid), dim3(NW * 64), 0, s, p);
   return hipGetLastError();
 }
 

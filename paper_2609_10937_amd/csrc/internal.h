@@ -61,6 +61,9 @@ struct FwdInstance {
   int q_blocks;   // query rows per wave / 16
   int n_waves;
   FwdLaunch launch;
+  // The same kernel as a persistent launch (one workgroup per CU running
+  // several query tiles back to back), or null when not compiled.
+  FwdLaunch launch_persist;
 };
 
 const FwdInstance* fwd_instances(int* count);
@@ -76,6 +79,9 @@ struct Prepared {
 };
 int prepare(const void* Q, const void* K, const void* V, void* O, int B, int H, int L, int d, float scale, int causal,
             int dtype, Prepared* out);
+// Enqueue the fused kernel of a prepared call (persistent when the plan's
+// launch grid differs from its grid).
+hipError_t launch_fused(const Prepared& pr, hipStream_t s);
 // Point the split partials of `p` into a workspace of at least Prepared::ws_bytes.
 void bind_workspace(FwdParams& p, void* ws, int d);
 

@@ -55,7 +55,7 @@ extern "C" int attn_fwd_noalloc(const void* Q, const void* K, const void* V, voi
     if (rc != ATTN_OK) return rc;
     bind_workspace(pr.p, ws, d);
   }
-  if (pr.inst->launch(pr.p, (unsigned)pr.rep.grid, s) != hipSuccess) return ATTN_E_HIP;
+  if (launch_fused(pr, s) != hipSuccess) return ATTN_E_HIP;
   if (pr.p.n_split > 1 && launch_combine(pr.p, d, dtype, s) != hipSuccess) return ATTN_E_HIP;
   return ATTN_OK;
 }

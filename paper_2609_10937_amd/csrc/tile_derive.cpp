@@ -211,6 +211,7 @@ int derive_tiles(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const a
   rep->n_split = (int32_t)n_split;
   rep->tiles_per_split = (int32_t)per;
   rep->grid = grid;
+  rep->launch_grid = grid;
   rep->vgpr_est = (int32_t)vgpr_estimate(hw, atom, op, t_q, t_kv, n_w);
   rep->wg_per_cu = (double)grid / hw->num_cus;
   rep->low_occupancy = grid < hw->num_cus;

@@ -94,6 +94,14 @@ CAUSAL_FEW_HEADS = (
 )
 WORKLOADS.update({w.name: w for w in CAUSAL_FEW_HEADS})
 
+# Many heads of short sequences (the fused kernel's persistent launch).
+SHORT_SEQUENCES = (
+    Workload("heads1024_l512_d128", 1, 1024, 512, 128, "bf16", False, 1.0, 1241),
+    Workload("heads512_l1024_d64", 1, 512, 1024, 64, "bf16", False, 1.0, 1242),
+    Workload("causal_heads512_l1024_d128", 1, 512, 1024, 128, "bf16", True, 1.0, 1243),
+)
+WORKLOADS.update({w.name: w for w in SHORT_SEQUENCES})
+
 
 def softmax_scale(d: int) -> float:
     """1/sqrt(d) evaluated in float32, returned as the Python float of that value."""

@@ -6,6 +6,7 @@ bit for bit with the oracle's model of the paper's rules (oracle/tile_model),
 which is itself pinned to Table 2.
 """
 import ctypes
+import itertools
 import json
 import os
 import re
@@ -212,6 +213,59 @@ def test_causal_pieces_by_hand(L, per, n_split, grid):
     assert (r.tiles_per_split, r.n_split, r.grid, r.binding) == (per, n_split, grid, b"CU")
 
 
+def _persistent_launch(r, L, d, causal, num_cus=256):
+    """The persistent-launch rule restated: no split, more query tiles than
+    CUs, d = 64 or 128 (the compiled variants), every query tile at least 4
+    key tiles long and on average at most 24, head offsets below 4 GiB."""
+    if d not in (64, 128) or r.n_split != 1 or r.grid <= num_cus or r.n_waves != 8:
+        return r.grid
+    if (L + r.tile_q) * d * 2 >= 1 << 32:
+        return r.grid
+    n_kv, n_qt = -(-L // r.t_kv), -(-L // r.tile_q)
+    tiles = [min(n_kv, -(-min(L, (qt + 1) * r.tile_q) // r.t_kv)) if causal else n_kv for qt in range(n_qt)]
+    return num_cus if min(tiles) >= 4 and sum(tiles) <= 24 * n_qt else r.grid
+
+
+def test_persistent_launch_by_hand():
+    hw = capi.attn_hw_desc_preset("gfx950")
+    bf = capi.ATTN_BF16
+    cases = [
+        # (B, H, L, d, causal) -> (grid, launch_grid)
+        ((1, 1024, 512, 128, 0), (2048, 256)),   # 8 key tiles per query tile
+        ((1, 128, 4096, 128, 0), (2048, 2048)),  # 64 key tiles: longer than 24
+        ((2, 16, 4096, 128, 1), (512, 512)),     # config 3: 4, 8, ..., 64 key tiles, mean 34
+        ((1, 512, 1024, 128, 1), (2048, 256)),   # causal: 4, 8, 12, 16, mean 10
+        ((8, 40, 200, 128, 0), (320, 256)),      # 4 key tiles, rows 200..255 past the sequence
+        ((1, 1000, 100, 128, 0), (1000, 1000)),  # 2 key tiles: too short for the switch
+        ((1, 64, 1024, 128, 0), (256, 256)),     # one round already
+        ((1, 512, 1024, 64, 0), (2048, 256)),    # d = 64: 8 key tiles of 128
+        ((1, 512, 1024, 64, 1), (2048, 2048)),   # d = 64 causal: the first query tile sees 2
+        ((1, 1024, 512, 256, 0), (4096, 4096)),  # d = 256: no persistent variant
+        ((1, 1024, 512, 96, 0), (2048, 2048)),   # d = 96: no persistent variant
+        ((1, 8, 1024, 128, 0), (256, 256)),      # split key ranges
+    ]
+    for (B, H, L, d, causal), (grid, launch) in cases:
+        r = capi.attn_fwd_plan(B, H, L, d, causal, bf, hw=hw)
+        assert (r.grid, r.launch_grid) == (grid, launch), (B, H, L, d, causal)
+    # The derivation alone always launches its own grid.
+    atom = capi.attn_atom_preset("bf16_16x16x32")
+    op = capi.attn_fwd_op(1, 1024, 512, 128, 0, bf)
+    rep = capi.attn_tile_derive(hw, atom, op)[1]
+    assert rep.launch_grid == rep.grid == 2048
+
+
+def test_persistent_launch_rule_over_shapes():
+    hw = capi.attn_hw_desc_preset("gfx950")
+    n = 0
+    for B, H, L, d, causal, dt in itertools.product((1, 2, 8), (1, 16, 40, 128, 512), (100, 200, 256, 300, 512, 700,
+                                                    1024, 1536, 2048, 4096), (64, 96, 128, 256), (0, 1),
+                                                   (capi.ATTN_BF16, capi.ATTN_F16)):
+        r = capi.attn_fwd_plan(B, H, L, d, causal, dt, hw=hw)
+        assert r.launch_grid == _persistent_launch(r, L, d, causal), (B, H, L, d, causal)
+        n += r.launch_grid != r.grid
+    assert n > 100
+
+
 def test_causal_halves_over_two_rounds_by_hand():
     """Four causal heads at L = 16384 fill one round of 256 CUs unsplit (64
     query tiles each), bound by the last tiles' 256 key tiles.  Halves of 128
@@ -318,11 +372,15 @@ def test_compiled_kernels_fit_without_scratch():
     with open(path) as f:
         res = json.load(f)
     fwd = {k: v for k, v in res.items() if "fwd_kernel" in k}
-    assert len(fwd) == 40
+    # 40 instances, and the persistent variant of the 8-wave one at d = 64 and
+    # 128 for both types.
+    assert len(fwd) == 44
+    persist = sorted(re.search(r"ILi(\d+)ELi(\d+)ELi\d+ELi\d+ELi8ELi5ELb1EE", k).groups() for k in fwd if "ELb1EE" in k)
+    assert persist == [("0", "128"), ("0", "64"), ("1", "128"), ("1", "64")]
     for name, r in res.items():
         assert r["scratch"] == 0, name
     for name, r in fwd.items():
-        nw = int(re.search(r"ILi\d+ELi\d+ELi\d+ELi\d+ELi(\d+)ELi\d+EE", name).group(1))
+        nw = int(re.search(r"ILi\d+ELi\d+ELi\d+ELi\d+ELi(\d+)ELi\d+ELb[01]EE", name).group(1))
         waves_per_simd = max(1, nw // 4)
         assert r["vgpr"] + r["agpr"] <= 512 // waves_per_simd, name
         assert r["lds"] <= 160 * 1024
@@ -340,7 +398,7 @@ def test_compiled_kernels_fit_without_scratch():
         assert est[d] <= 256 < capi.attn_vgpr_estimate(hw, atom, op, t_q + 16, t_kv, 8), d
         r = capi.attn_fwd_plan(1, 1, 16384, d, 0, capi.ATTN_BF16, hw=hw)
         assert (r.t_kv, r.t_q_wave, r.vgpr_est) == (t_kv, t_q, est[d])
-        tag = f"ILi0ELi{d}ELi{t_kv}ELi{t_q // 16}ELi8ELi5EE"
+        tag = f"ILi0ELi{d}ELi{t_kv}ELi{t_q // 16}ELi8ELi5ELb0EE"
         comp = [v for k, v in fwd.items() if tag in k][0]
         assert comp["scratch"] == 0 and comp["vgpr"] + comp["agpr"] <= 256
     # d = 128, 32 rows: 32 (Q) + 32 (S) + 64 (O) + 16 (P) + 2 x 7 (statistics)

@@ -290,6 +290,37 @@ def test_many_heads_small_l(causal):
     _gpu.assert_close(_gpu.download(o, "bf16"), ref, "bf16", "many heads")
 
 
+PERSISTENT = [
+    (1, 300, 700, 128, False, "bf16"),  # plain order, a ragged last query tile (rows 700..767 dropped)
+    (2, 160, 512, 64, False, "f16"),    # d = 64
+    (1, 520, 256, 128, True, "bf16"),   # causal query tiles of exactly 4 key tiles: switches 4 steps apart
+    (1, 288, 1024, 128, True, "f16"),   # causal, 4 to 16 key tiles per query tile
+    (4, 64, 512, 128, False, "bf16"),   # the XCD-grouped order
+]
+
+
+@pytest.mark.parametrize("B,H,L,d,causal,dtype", PERSISTENT)
+def test_persistent_launch_all_rows(B, H, L, d, causal, dtype):
+    """Plans that run as a persistent launch (one workgroup per CU taking a
+    fixed list of query tiles back to back): every row against the oracle,
+    into an output first filled with NaN, so that a row no workgroup wrote
+    fails."""
+    import torch
+    dt = capi.ATTN_BF16 if dtype == "bf16" else capi.ATTN_F16
+    plan = capi.attn_fwd_plan(B, H, L, d, causal, dt)
+    assert plan.launch_grid < plan.grid, "shape expected to run persistent"
+    print(f"case persistent B{B} H{H} L{L} d{d} causal{int(causal)} {dtype} grid {plan.grid} "
+          f"launch {plan.launch_grid}", flush=True)
+    q, k, v = inputs.make_qkv(B, H, L, d, dtype, seed=L * 7 + H)
+    s = inputs.softmax_scale(d)
+    tq, tk, tv = (_gpu.upload(x, dtype) for x in (q, k, v))
+    o = torch.full_like(tq, float("nan"))
+    capi.attn_fwd(tq, tk, tv, o, s, causal)
+    torch.cuda.synchronize()
+    ref = A.attention(_f64(q, dtype), _f64(k, dtype), _f64(v, dtype), s, causal)
+    _gpu.assert_close(_gpu.download(o, dtype), ref, dtype, "persistent")
+
+
 # ------------------------------------------------------------ invariants on the GPU
 
 def test_gpu_invariants():
