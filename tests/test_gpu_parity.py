@@ -321,6 +321,47 @@ def test_persistent_launch_all_rows(B, H, L, d, causal, dtype):
     _gpu.assert_close(_gpu.download(o, dtype), ref, dtype, "persistent")
 
 
+def _persistent_random_cases(n=12, seed=4242):
+    """Seeded shapes whose plans run persistent: d = 64 or 128, causal or not,
+    either type, L from 200 to 1600 (ragged last query tiles included), and
+    enough heads for 260 to 700 query tiles (planned on the gfx950 preset)."""
+    rng = np.random.default_rng(seed)
+    hw = capi.attn_hw_desc_preset("gfx950")
+    out = []
+    while len(out) < n:
+        d = int(rng.choice([64, 128]))
+        causal = bool(rng.integers(0, 2))
+        dtype = str(rng.choice(["bf16", "f16"]))
+        L = int(rng.integers(200, 1601))
+        n_qt = -(-L // 256)
+        bh = int(rng.integers(-(-260 // n_qt), 700 // n_qt + 1))
+        B = int(rng.choice([1, 2])) if bh % 2 == 0 else 1
+        H = bh // B
+        r = capi.attn_fwd_plan(B, H, L, d, causal, capi.ATTN_BF16 if dtype == "bf16" else capi.ATTN_F16, hw=hw)
+        if r.launch_grid < r.grid:
+            out.append((B, H, L, d, causal, dtype))
+    return out
+
+
+@pytest.mark.parametrize("B,H,L,d,causal,dtype", _persistent_random_cases())
+def test_persistent_random_shapes(B, H, L, d, causal, dtype):
+    """Seeded persistent plans: every row against the oracle, into an output
+    first filled with NaN."""
+    import torch
+    dt = capi.ATTN_BF16 if dtype == "bf16" else capi.ATTN_F16
+    plan = capi.attn_fwd_plan(B, H, L, d, causal, dt)
+    assert plan.launch_grid < plan.grid
+    print(f"case persistent-random B{B} H{H} L{L} d{d} causal{int(causal)} {dtype} grid {plan.grid}", flush=True)
+    q, k, v = inputs.make_qkv(B, H, L, d, dtype, seed=L * 13 + H * 3 + d)
+    s = inputs.softmax_scale(d)
+    tq, tk, tv = (_gpu.upload(x, dtype) for x in (q, k, v))
+    o = torch.full_like(tq, float("nan"))
+    capi.attn_fwd(tq, tk, tv, o, s, causal)
+    torch.cuda.synchronize()
+    ref = A.attention(_f64(q, dtype), _f64(k, dtype), _f64(v, dtype), s, causal)
+    _gpu.assert_close(_gpu.download(o, dtype), ref, dtype, "persistent random")
+
+
 # ------------------------------------------------------------ invariants on the GPU
 
 def test_gpu_invariants():
@@ -496,9 +537,11 @@ def test_partial_then_merge_equals_fused_causal_pieces(B, H, L, d, dtype):
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
 
 
-@pytest.mark.parametrize("name", ["single_head_l16384_d128", "h8_l1024_d128", "tiny_f16_l128_d64"])
+@pytest.mark.parametrize("name", ["single_head_l16384_d128", "h8_l1024_d128", "tiny_f16_l128_d64",
+                                  "heads1024_l512_d128"])
 def test_partial_then_merge_equals_fused(name):
-    """attn_fwd_partial + attn_fwd_merge with a caller workspace == attn_fwd, bit for bit."""
+    """attn_fwd_partial + attn_fwd_merge with a caller workspace == attn_fwd, bit
+    for bit (the last workload runs as a persistent launch)."""
     w = inputs.WORKLOADS[name]
     print(f"case partial+merge {name}", flush=True)
     q, k, v = (_gpu.upload(x, w.dtype) for x in inputs.workload_inputs(w))
