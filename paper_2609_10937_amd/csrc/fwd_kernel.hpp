@@ -450,7 +450,8 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   };
 
   // Persistent launch (PERSIST: one workgroup per CU, without split key
-  // ranges).  The workgroups b = 8 i + x that the order above puts on XCD x
+  // ranges, so the order above has one workgroup per query tile, BH n_qt in
+  // all).  The workgroups b = 8 i + x that the order above puts on XCD x
   // become units of work shared by the launch's S = gridDim.x / 8 workgroups
   // on that XCD, in rounds taken snake-wise: in round r slot s takes item
   // r S + s when r is even and r S + S - 1 - s when r is odd, so that a

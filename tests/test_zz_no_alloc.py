@@ -48,6 +48,13 @@ def test_noalloc_without_split_and_refusal():
     print(f"case noalloc {w.name} (no split)", flush=True)
     _, a, b = _run_both(w)
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    # no split, a persistent launch
+    w = inputs.WORKLOADS["heads1024_l512_d128"]
+    plan = capi.attn_fwd_plan(w.B, w.H, w.L, w.d, w.causal, capi.ATTN_BF16)
+    assert plan.launch_grid < plan.grid
+    print(f"case noalloc {w.name} (persistent)", flush=True)
+    _, a, b = _run_both(w)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
     # one head, L = 20000, d = 96: 9 key splits, 36.0 MB of partials
     B, H, L, d = 1, 1, 20000, 96
     nb = capi.attn_fwd_workspace_bytes(B, H, L, d, False, capi.ATTN_BF16)
