@@ -184,23 +184,20 @@ def derive(hw, atom, op, st):
         # min(n_kv, ceil(min(L, (qt+1) tile_q) / t_kv)) key tiles, so fixed
         # key ranges leave the early tiles' later splits empty and give the
         # last tiles all the work.  Instead each query tile's own key tiles
-        # are cut into pieces of per = c m tiles (c = tile_q / t_kv, whole
-        # query tiles then have whole pieces per c), only non-empty pieces
-        # are workgroups, and per is the smallest such size -- with at most
-        # max_split pieces per tile -- whose workgroups fit one round of CUs;
-        # kept when that one round is shorter than the fixed ranges' rounds,
-        # each workgroup costing its fixed cost plus its key tiles.
-        c = tile_q // t_kv
-        m = max(1, _cdiv(n_kv, c * st.max_split))
+        # are cut into pieces of per tiles, only non-empty pieces are
+        # workgroups, and per is the smallest size -- with at most max_split
+        # pieces per tile -- whose workgroups fit one round of CUs; kept when
+        # that one round is shorter than the fixed ranges' rounds, each
+        # workgroup costing its fixed cost plus its key tiles.
+        p_per = _cdiv(n_kv, st.max_split)
         while True:
-            p_per = c * m
             pieces = 0
             for qt in range(n_qt):
                 seen = min(n_kv, _cdiv(min(op.L, (qt + 1) * tile_q), t_kv))
                 pieces += _cdiv(seen, p_per)
             if heads * pieces <= hw.num_cus or p_per >= n_kv:
                 break
-            m += 1
+            p_per += 1
         c0 = st.wg_fixed_steps
         if c0 + p_per < _cdiv(grid, hw.num_cus) * (c0 + per):
             per = p_per

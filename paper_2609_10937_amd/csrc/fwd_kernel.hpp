@@ -390,18 +390,17 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
   if constexpr (TILE_Q % TKV == 0) {
     if (order == kOrderPieces) {
       // Causal with split key ranges: query tile qt sees its first n_kv(qt)
-      // key tiles, cut into pieces of P = tiles_per_split = C m tiles
-      // (C = TILE_Q / TKV); a whole query tile qt < n_qt - 1 sees C (qt + 1)
-      // tiles and so has ceil((qt + 1) / m) pieces.  Heads run fastest; then
-      // the last query tile's pieces (whole tile or not); then, piece-major,
-      // the first piece of every whole tile (heaviest first), then every
-      // second piece, ...: piece k exists for the nf - k m whole tiles
-      // qt >= k m (nf = n_qt - 1), so pieces 0 .. k-1 take
-      // G(k) = k nf - m k (k - 1) / 2 places.  Consecutive workgroups go to
-      // consecutive XCDs, and this order gives each XCD a like mix of long
-      // and short pieces.
+      // key tiles, cut into pieces of P = tiles_per_split tiles.  A whole
+      // query tile qt < n_qt - 1 sees C (qt + 1) tiles (C = TILE_Q / TKV), so
+      // its piece k exists when C (qt + 1) > k P, that is for the
+      // nf - floor(k P / C) whole tiles qt >= floor(k P / C) (nf = n_qt - 1).
+      // Heads run fastest; then the last query tile's pieces (whole tile or
+      // not); then, piece-major, the first piece of every whole tile
+      // (heaviest first), then every second piece, ...  Consecutive
+      // workgroups go to consecutive XCDs, and this order gives each XCD a
+      // like mix of long and short pieces.
       constexpr int C = TILE_Q / TKV;
-      const int P = p.tiles_per_split, m = P / C;
+      const int P = p.tiles_per_split;
       head = blockIdx.x % p.BH;
       const int j = blockIdx.x / p.BH;
       const int n_last = (min(L, p.n_qt * TILE_Q) + TKV - 1) / TKV;  // key tiles the last query tile sees
@@ -410,15 +409,16 @@ __global__ void __launch_bounds__(NW * 64) fwd_kernel(const FwdParams p) {
         qt = p.n_qt - 1;
         split = j;
       } else {
-        const int jp = j - a_last, nf = p.n_qt - 1;
-        const int K = (nf + m - 1) / m;  // pieces of the longest whole tile
-        const float hb = (float)nf + 0.5f * (float)m;
-        const float disc = fmaxf(0.f, hb * hb - 2.f * (float)m * (float)jp);
-        int k = (int)((hb - __builtin_sqrtf(disc)) / (float)m);
-        k = min(max(k, 0), K - 1);
-        while (k + 1 < K && (k + 1) * nf - m * (k + 1) * k / 2 <= jp) ++k;
-        while (k > 0 && k * nf - m * k * (k - 1) / 2 > jp) --k;
-        qt = nf - 1 - (jp - (k * nf - m * k * (k - 1) / 2));
+        // The host launches exactly the pieces (at most n_split per tile), so
+        // jp falls within piece k before k reaches n_split - 1.
+        const int nf = p.n_qt - 1;
+        int jp = j - a_last, k = 0;
+        for (; k + 1 < p.n_split; ++k) {
+          const int cnt = nf - (k * P) / C;
+          if (jp < cnt) break;
+          jp -= cnt;
+        }
+        qt = max(0, nf - 1 - jp);
         split = k;
       }
       placed = true;

@@ -167,15 +167,15 @@ int derive_tiles(const attn_hw_desc_t* hw, const attn_mfma_atom_t* atom, const a
     // Causal: query tile qt sees only its first min(n_kv, ceil(min(L,
     // (qt+1) tile_q) / t_kv)) key tiles, so fixed key ranges would leave the
     // early tiles' later splits empty and give the last tiles all the work.
-    // Each query tile's own key tiles are cut into pieces of per = c m tiles
-    // (c = tile_q / t_kv), only non-empty pieces are workgroups, and per is
-    // the smallest such size (at most max_split pieces per tile) whose
-    // workgroups fit one round of CUs.
-    const int64_t c = tile_q / t_kv;
-    int64_t m = std::max<int64_t>(1, cdiv(n_kv, c * op->max_split));
-    int64_t pieces = 0, p_per = 0;
-    for (;; ++m) {
-      p_per = c * m;
+    // Each query tile's own key tiles are cut into pieces of p_per tiles,
+    // only non-empty pieces are workgroups, and p_per is the smallest size
+    // (at most max_split pieces per tile) whose workgroups fit one round of
+    // CUs.  The search starts at the bound that the pieces of all query
+    // tiles, at least their key tiles over p_per, fit the CUs.
+    const int64_t seen = causal_pieces(op->L, tile_q, t_kv, n_qt, n_kv, 1);  // key tiles over all query tiles
+    int64_t p_per = std::max(cdiv(n_kv, op->max_split), cdiv(heads * seen, hw->num_cus));
+    int64_t pieces = 0;
+    for (;; ++p_per) {
       pieces = causal_pieces(op->L, tile_q, t_kv, n_qt, n_kv, p_per);
       if (heads * pieces <= hw->num_cus || p_per >= n_kv) break;
     }

@@ -194,19 +194,20 @@ def test_split_count_by_rounds(shape, split, grid):
 
 
 @pytest.mark.parametrize("L,per,n_split,grid", [
-    # 64 query tiles of 256 rows, 256 key tiles, 4 key tiles per query tile:
-    # pieces of 4m tiles, m >= ceil(256 / (4 * 16)) = 4.  Query tile qt has
-    # ceil((qt + 1) / m) pieces: m = 9 gives 9 (1 + ... + 7) + 8 = 260 > 256,
-    # m = 10 gives 10 (1 + ... + 6) + 4 * 7 = 238
-    (16384, 40, 7, 238),
-    # 32 query tiles, 128 key tiles, m >= 2: m = 2 gives 2 (1 + ... + 16) =
-    # 272 > 256, m = 3 gives 3 (1 + ... + 10) + 2 * 11 = 187
-    (8192, 12, 11, 187),
+    # 64 query tiles of 256 rows, 256 key tiles; query tile x = qt + 1 sees
+    # 4x key tiles (8320 in all), so a piece holds at least
+    # max(256 / 16, 8320 / 256) -> 33 tiles.  Pieces of 36: ceil(4x / 36) is
+    # 1..7 for nine x each and 8 for x = 64: 9 (1 + ... + 7) + 8 = 260 > 256;
+    # of 37: 1, 2, 3 for nine x each, 4 for ten, 5, 6, 7 for nine each:
+    # 9 + 18 + 27 + 40 + 45 + 54 + 63 = 256
+    (16384, 37, 7, 256),
+    # 32 query tiles, 128 key tiles, 2112 in all: at least 9 per piece; of
+    # 9: ceil(4x / 9) for x = 1..32 adds up to 249
+    (8192, 9, 15, 249),
 ])
 def test_causal_pieces_by_hand(L, per, n_split, grid):
     """Causal single heads: each query tile's own key tiles are cut into the
-    smallest pieces (whole multiples of the 4 key tiles a query tile adds)
-    whose count fits one round of 256 CUs (worked by hand)."""
+    smallest pieces whose count fits one round of 256 CUs (worked by hand)."""
     hw = capi.attn_hw_desc_preset("gfx950")
     r = capi.attn_fwd_plan(1, 1, L, 128, 1, capi.ATTN_BF16, hw=hw)
     assert (r.tile_q, r.t_kv) == (256, 64)

@@ -144,19 +144,18 @@ def test_budgets_alignment_maximality(hw, atom, op, st):
     if op.causal and rep["grid"] < op.B * op.H * n_qt * rep["n_split"]:
         # causal pieces: the grid counts the non-empty pieces of every query
         # tile's own key range, fits one round, and one key tile less per
-        # piece (keeping whole query tiles in whole pieces) would not
+        # piece would not
         c = rep["tile_q"] // rep["t_kv"]
-        assert per % c == 0
         def pieces(pp):
             return sum(-(-min(n_kv, -(-min(op.L, (qt + 1) * rep["tile_q"]) // rep["t_kv"])) // pp)
                        for qt in range(n_qt))
         heads = op.B * op.H
         assert rep["grid"] == heads * pieces(per)
         if heads * n_qt < hw.num_cus:
-            # one round, and one step of c key tiles less per piece would not fit it
+            # one round, and one key tile less per piece would not fit it
             assert rep["grid"] <= hw.num_cus
-            if per > c and -(-n_kv // (per - c)) <= st.max_split:
-                assert heads * pieces(per - c) > hw.num_cus
+            if per > 1 and -(-n_kv // (per - 1)) <= st.max_split:
+                assert heads * pieces(per - 1) > hw.num_cus
         else:
             # filled between one and two rounds unsplit: halves of at least 32
             # key tiles that fit two rounds
