@@ -214,6 +214,48 @@ def test_causal_pieces_by_hand(L, per, n_split, grid):
     assert (r.tiles_per_split, r.n_split, r.grid, r.binding) == (per, n_split, grid, b"CU")
 
 
+def _piece_of(b, BH, n_qt, L, tile_q, t_kv, P, n_split):
+    """The fused kernel's placement of workgroup b of a causal-pieces launch,
+    restated: heads fastest, the last query tile's pieces first, then
+    piece-major over the whole query tiles, heaviest first."""
+    C = tile_q // t_kv
+    head, j = b % BH, b // BH
+    n_last = -(-min(L, n_qt * tile_q) // t_kv)
+    a_last = -(-n_last // P)
+    if j < a_last:
+        return head, n_qt - 1, j
+    nf, jp, k = n_qt - 1, j - a_last, 0
+    while k + 1 < n_split:
+        cnt = nf - (k * P) // C
+        if jp < cnt:
+            break
+        jp -= cnt
+        k += 1
+    return head, max(0, nf - 1 - jp), k
+
+
+def test_causal_piece_placement_covers_every_piece_once():
+    """For every plan that cuts causal query tiles into pieces, the kernel's
+    placement maps the launched workgroups one to one onto the non-empty
+    pieces (query tile qt has ceil(n_kv(qt) / P) of them)."""
+    hw = capi.attn_hw_desc_preset("gfx950")
+    n = 0
+    for H, L, d in itertools.product((1, 2, 3), (1000, 3000, 5000, 8192, 12345, 16384, 20000, 32768),
+                                     (64, 96, 128, 256)):
+        r = capi.attn_fwd_plan(1, H, L, d, 1, capi.ATTN_BF16, hw=hw)
+        n_qt = -(-L // r.tile_q)
+        if r.n_split == 1 or r.grid == H * n_qt * r.n_split:
+            continue  # no pieces
+        n_kv = -(-L // r.t_kv)
+        P = r.tiles_per_split
+        want = {(h, qt, k) for h in range(H) for qt in range(n_qt)
+                for k in range(-(-min(n_kv, -(-min(L, (qt + 1) * r.tile_q) // r.t_kv)) // P))}
+        got = [_piece_of(b, H, n_qt, L, r.tile_q, r.t_kv, P, r.n_split) for b in range(r.grid)]
+        assert len(got) == len(set(got)) == len(want) and set(got) == want, (H, L, d)
+        n += 1
+    assert n >= 20
+
+
 def _persistent_launch(r, L, d, causal, num_cus=256):
     """The persistent-launch rule restated: no split, more query tiles than
     CUs, d = 64 or 128 (the compiled variants), every query tile at least 4

@@ -362,6 +362,43 @@ def test_persistent_random_shapes(B, H, L, d, causal, dtype):
     _gpu.assert_close(_gpu.download(o, dtype), ref, dtype, "persistent random")
 
 
+def _pieces_random_cases(n=8, seed=5150):
+    """Seeded causal shapes of one or two heads whose plans cut query tiles
+    into pieces: every head dimension, either type, L from 2000 to 20000
+    (12000 at d = 256), planned on the gfx950 preset."""
+    rng = np.random.default_rng(seed)
+    hw = capi.attn_hw_desc_preset("gfx950")
+    out = []
+    while len(out) < n:
+        d = int(rng.choice([64, 96, 128, 256]))
+        H = int(rng.integers(1, 3))
+        L = int(rng.integers(2000, 12001 if d == 256 else 20001))
+        dtype = str(rng.choice(["bf16", "f16"]))
+        r = capi.attn_fwd_plan(1, H, L, d, 1, capi.ATTN_BF16 if dtype == "bf16" else capi.ATTN_F16, hw=hw)
+        if r.n_split > 1 and r.grid < H * (-(-L // r.tile_q)) * r.n_split:
+            out.append((H, L, d, dtype))
+    return out
+
+
+@pytest.mark.parametrize("H,L,d,dtype", _pieces_random_cases())
+def test_causal_pieces_random_shapes(H, L, d, dtype):
+    """Seeded causal-pieces plans: every row against the oracle, into an
+    output first filled with NaN (a piece no workgroup ran leaves NaN)."""
+    import torch
+    dt = capi.ATTN_BF16 if dtype == "bf16" else capi.ATTN_F16
+    plan = capi.attn_fwd_plan(1, H, L, d, True, dt)
+    print(f"case pieces-random H{H} L{L} d{d} {dtype} P {plan.tiles_per_split} slots {plan.n_split} "
+          f"grid {plan.grid}", flush=True)
+    q, k, v = inputs.make_qkv(1, H, L, d, dtype, seed=L + 31 * d + H)
+    s = inputs.softmax_scale(d)
+    tq, tk, tv = (_gpu.upload(x, dtype) for x in (q, k, v))
+    o = torch.full_like(tq, float("nan"))
+    capi.attn_fwd(tq, tk, tv, o, s, True)
+    torch.cuda.synchronize()
+    ref = A.attention(_f64(q, dtype), _f64(k, dtype), _f64(v, dtype), s, True)
+    _gpu.assert_close(_gpu.download(o, dtype), ref, dtype, "pieces random")
+
+
 # ------------------------------------------------------------ invariants on the GPU
 
 def test_gpu_invariants():
