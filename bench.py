@@ -591,7 +591,8 @@ def main():
                    "inputs": "N(0,1) float32 rounded to bf16, seed 1004",
                    "tiles": {"t_kv": plan.t_kv, "t_q_wave": plan.t_q_wave, "n_waves": plan.n_waves,
                              "tile_q": plan.tile_q, "n_split": plan.n_split, "grid": plan.grid,
-                             "vgpr_est": plan.vgpr_est, "binding": plan.binding.decode()},
+                             "launch_grid": plan.launch_grid, "vgpr_est": plan.vgpr_est,
+                             "binding": plan.binding.decode()},
                    "device": {"num_cus": desc.num_cus, "lds_bytes": desc.lds_bytes,
                               "clock_ghz": desc.clock_ghz}},
         "pct_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
