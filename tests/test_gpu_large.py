@@ -2,9 +2,10 @@
 
 * Tensors past 4 GiB (more than 2^31 elements): heads whose byte offsets no
   32-bit integer holds, through the plain launch and through the persistent
-  one.  Every head copies one of seven seeded base heads (head f takes base
-  f mod 7; 4096 mod 7 = 1, so the heads 2^k apart that a wrapped 32-bit
-  offset would confuse hold different data).  The kernel's arithmetic for a
+  one, at d = 128 (bf16) and d = 64 (f16).  Every head copies one of seven
+  seeded base heads (head f takes base f mod 7; no power of two is a
+  multiple of 7, so the heads 2^k apart that a wrapped 32-bit offset would
+  confuse hold different data).  The kernel's arithmetic for a
   head does not depend on where the head sits, so every head's output must
   equal its base's bit for bit, and the seven bases are compared row by row
   with the float64 oracle: all rows of all heads are checked.
@@ -32,25 +33,26 @@ def _f64(bits, dtype):
 
 
 BEYOND_4GIB = [
-    # B, H, L, causal, persistent launch expected
-    (2, 2050, 4096, False, False),
-    (2, 2050, 4096, True, False),
-    (1, 32800, 512, False, True),
-    (4, 8200, 512, True, True),
+    # B, H, L, d, causal, type, persistent launch expected
+    (2, 2050, 4096, 128, False, "bf16", False),
+    (2, 2050, 4096, 128, True, "bf16", False),
+    (1, 32800, 512, 128, False, "bf16", True),
+    (4, 8200, 512, 128, True, "bf16", True),
+    (2, 4100, 4096, 64, True, "f16", False),
+    (1, 65600, 512, 64, False, "f16", True),
 ]
 
 
-@pytest.mark.parametrize("B,H,L,causal,persistent", BEYOND_4GIB)
-def test_tensors_beyond_4gib_all_heads(B, H, L, causal, persistent):
-    d, dtype = 128, "bf16"
+@pytest.mark.parametrize("B,H,L,d,causal,dtype,persistent", BEYOND_4GIB)
+def test_tensors_beyond_4gib_all_heads(B, H, L, d, causal, dtype, persistent):
     BH = B * H
     assert BH * L * d > 1 << 31
-    plan = capi.attn_fwd_plan(B, H, L, d, causal, capi.ATTN_BF16)
+    plan = capi.attn_fwd_plan(B, H, L, d, causal, capi.ATTN_BF16 if dtype == "bf16" else capi.ATTN_F16)
     assert plan.n_split == 1
     assert (plan.launch_grid < plan.grid) == persistent
-    print(f"case beyond_4gib B{B} H{H} L{L} d{d} causal{int(causal)} grid {plan.grid} "
+    print(f"case beyond_4gib B{B} H{H} L{L} d{d} causal{int(causal)} {dtype} grid {plan.grid} "
           f"launch {plan.launch_grid}", flush=True)
-    q, k, v = inputs.make_qkv(1, N_BASE, L, d, dtype, seed=1301 + L + int(causal))
+    q, k, v = inputs.make_qkv(1, N_BASE, L, d, dtype, seed=1301 + L + d + int(causal))
     idx = torch.arange(BH, device="cuda") % N_BASE
     tq, tk, tv = (_gpu.upload(x, dtype)[0][idx].view(B, H, L, d) for x in (q, k, v))
     o = torch.full_like(tq, float("nan"))
