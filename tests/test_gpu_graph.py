@@ -80,3 +80,51 @@ def test_graph_replays_match_eager(name, B, H, L, d, causal, dtype, entry):
         assert torch.equal(other.view(torch.int16), eager[(rep + 1) % 2].view(torch.int16))
     del g
     torch.cuda.synchronize()
+
+
+def test_capture_refuses_to_grow_the_workspace():
+    """A split call captured on a stream that has no workspace yet must not
+    allocate under capture: attn_fwd returns ATTN_E_WORKSPACE and records
+    nothing; after the capture ends the same call runs eagerly and matches
+    the call on the default stream."""
+    import ctypes
+    hip = ctypes.CDLL("libamdhip64.so")
+    hip.hipStreamBeginCapture.argtypes = [ctypes.c_void_p, ctypes.c_int]
+    hip.hipStreamEndCapture.argtypes = [ctypes.c_void_p, ctypes.POINTER(ctypes.c_void_p)]
+    hip.hipGraphDestroy.argtypes = [ctypes.c_void_p]
+    hip.hipStreamCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+    hip.hipStreamSynchronize.argtypes = [ctypes.c_void_p]
+    hip.hipStreamDestroy.argtypes = [ctypes.c_void_p]
+    B, H, L, d, dtype = 1, 1, 4096, 128, "bf16"
+    assert capi.attn_fwd_plan(B, H, L, d, False, capi.ATTN_BF16).n_split > 1
+    print(f"case graph capture refusal B{B} H{H} L{L} d{d}", flush=True)
+    s = inputs.softmax_scale(d)
+    tq, tk, tv = (_gpu.upload(x, dtype) for x in inputs.make_qkv(B, H, L, d, dtype, seed=1451))
+    o_ref = torch.empty_like(tq)
+    capi.attn_fwd(tq, tk, tv, o_ref, s, False)
+    torch.cuda.synchronize()
+    # a stream of its own (torch's streams come from a pool that earlier
+    # calls may have used, and their workspaces would already fit)
+    handle = ctypes.c_void_p()
+    assert hip.hipStreamCreate(ctypes.byref(handle)) == 0
+    fresh = handle.value
+    try:
+        o = torch.full_like(tq, float("nan"))
+        torch.cuda.synchronize()
+        assert hip.hipStreamBeginCapture(fresh, 0) == 0  # global capture mode
+        try:
+            with pytest.raises(capi.AttnError) as e:
+                capi.attn_fwd(tq, tk, tv, o, s, False, stream=fresh)
+        finally:
+            graph = ctypes.c_void_p()
+            end = hip.hipStreamEndCapture(fresh, ctypes.byref(graph))
+        assert end == 0
+        if graph.value:
+            hip.hipGraphDestroy(graph)
+        assert e.value.status == capi.CODE["ATTN_E_WORKSPACE"]
+        capi.attn_fwd(tq, tk, tv, o, s, False, stream=fresh)
+        assert hip.hipStreamSynchronize(fresh) == 0
+        assert torch.equal(o.view(torch.int16), o_ref.view(torch.int16))
+    finally:
+        torch.cuda.synchronize()
+        hip.hipStreamDestroy(fresh)
