@@ -63,12 +63,19 @@ def test_tensors_beyond_4gib_all_heads(B, H, L, d, causal, dtype, persistent):
     of = o.view(BH, L, d).view(torch.int16)
     for r in range(N_BASE):
         assert torch.equal(of[r::N_BASE], of[r].expand(of[r::N_BASE].shape)), f"heads of base {r} differ"
+    # the heads on either side of the first one past 2^31 elements (2^32
+    # bytes) and the last head, compared with the oracle directly: their
+    # inputs are those of base f mod 7
+    hb = (1 << 31) // (L * d)
+    far = [hb - 1, hb, hb + 1, BH - 1]
     got = _gpu.download(o.view(BH, L, d)[:N_BASE], dtype)
+    got_far = _gpu.download(o.view(BH, L, d)[torch.tensor(far, device="cuda")], dtype)
     del o, of
     torch.cuda.empty_cache()
     ref = A.attention(_f64(q, dtype), _f64(k, dtype), _f64(v, dtype), s, causal)[0]
     mx, mn = _gpu.assert_close(got, ref, dtype, "beyond 4 GiB")
-    print(f"  max_abs {mx:.3e} mean_abs {mn:.3e} over {N_BASE} base heads", flush=True)
+    _gpu.assert_close(got_far, ref[[f % N_BASE for f in far]], dtype, f"heads {far}")
+    print(f"  max_abs {mx:.3e} mean_abs {mn:.3e} over {N_BASE} base heads; heads {far} checked too", flush=True)
 
 
 @pytest.mark.parametrize("causal", [False, True])
