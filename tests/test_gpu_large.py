@@ -2,10 +2,10 @@
 
 * Tensors past 4 GiB (more than 2^31 elements): heads whose byte offsets no
   32-bit integer holds, through the plain launch and through the persistent
-  one, at d = 128 (bf16) and d = 64 (f16).  Every head copies one of seven
-  seeded base heads (head f takes base f mod 7; no power of two is a
-  multiple of 7, so the heads 2^k apart that a wrapped 32-bit offset would
-  confuse hold different data).  The kernel's arithmetic for a
+  one, at every head dimension (bf16, and f16 at d = 64).  Every head copies
+  one of seven seeded base heads (head f takes base f mod 7; no power of two
+  is a multiple of 7, so the heads 2^k apart that a wrapped 32-bit offset
+  would confuse hold different data).  The kernel's arithmetic for a
   head does not depend on where the head sits, so every head's output must
   equal its base's bit for bit, and the seven bases are compared row by row
   with the float64 oracle: all rows of all heads are checked.
@@ -40,6 +40,8 @@ BEYOND_4GIB = [
     (4, 8200, 512, 128, True, "bf16", True),
     (2, 4100, 4096, 64, True, "f16", False),
     (1, 65600, 512, 64, False, "f16", True),
+    (2, 1030, 4096, 256, False, "bf16", False),
+    (2, 2740, 4096, 96, True, "bf16", False),
 ]
 
 
